@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of the SnapStream hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch: snap_compress of
+every (layer, sequence) from prompts resident in HBM, then `decode_steps`
+decode steps, each running snap_cache_append + snap_decode_attn for every
+layer and one snap_advance.  Inputs (prompts and every decode step's q/k/v)
+are generated before the timed region.
+
+Prints ONE JSON line.  `value` is decoded tokens per second of the whole step
+(compression included); the decode-only rate, the decode-attention HBM GB/s
+and the per-(sequence, layer) snap_compress latency are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
+PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
+    ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--event-every", type=int, default=16, help="time decode calls of every n-th decode step")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the hot path shards by "
+              "KV head or by slot with no exchange; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2511_03092_amd as snap
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    if wl.slots is not None:
+        print("the continuous-batching workload is benchmarked by its own driver loop (not yet wired here)",
+              file=sys.stderr)
+        sys.exit(2)
+    layers = args.layers or wl.layers
+    dsteps = wl.decode_steps if args.decode_steps is None else args.decode_steps
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
+    p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
+                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype])
+    n = wl.batch
+    lengths = synth.draw_lengths(wl, 0, n)
+    max_len = max(lengths)
+    B = p.budget
+    kvt = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}[wl.kv_dtype]
+
+    # ---- resident inputs and caches (untimed)
+    t_setup = time.time()
+    prompts, caches, dec = [], [], []
+    for l in range(layers):
+        q, k, v = synth.prefill_batch(wl, l, lengths, device=dev, max_len=max_len)
+        prompts.append((q, k, v))
+        ck = torch.zeros((n, wl.n_kv_heads, B, wl.d_qk), dtype=kvt, device=dev)
+        cv = None if wl.v_in_k else torch.zeros((n, wl.n_kv_heads, B, wl.d_v), dtype=kvt, device=dev)
+        caches.append((ck, cv, snap.cache_struct(ck, cv)))
+        dec.append(synth.decode_inputs_all(wl, l, max(dsteps, 1), lengths, device=dev))
+    pos = torch.zeros((n,), dtype=torch.int32, device=dev)
+    ntop = torch.zeros((n,), dtype=torch.int32, device=dev)
+    slots = torch.arange(n, dtype=torch.int32, device=dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    wsc = snap.workspace(snap.snap_compress_workspace(p, n, max_len), dev)
+    wsd = snap.workspace(snap.snap_decode_workspace(p, n), dev)
+    out = torch.empty((n, wl.n_q_heads, wl.d_v), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+
+    # ---- one step
+    def step(timing):
+        for l in range(layers):
+            q, k, v = prompts[l]
+            if timing is not None:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            snap.snap_compress(p, caches[l][2], pos, ntop, slots, lens, q, k, v, wsc, stream=sptr)
+            if timing is not None:
+                e1 = torch.cuda.Event(enable_timing=True)
+                e1.record(stream)
+                timing["compress"].append((e0, e1))
+        for t in range(dsteps):
+            sample = timing is not None and (t % args.event_every == 0)
+            for l in range(layers):
+                qd, kd, vd = dec[l]
+                snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t], stream=sptr)
+                if sample:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                snap.snap_decode_attn(p, caches[l][2], pos, ntop, slots, qd[t], out, wsd, stream=sptr)
+                if sample:
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e1.record(stream)
+                    timing["decode"].append((e0, e1))
+            snap.snap_advance(pos, slots, stream=sptr)
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    timing = {"compress": [], "decode": []}
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(timing)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    comp_ms = sum(a.elapsed_time(b) for a, b in timing["compress"]) / max(len(timing["compress"]), 1)
+    dec_ms = sum(a.elapsed_time(b) for a, b in timing["decode"]) / max(len(timing["decode"]), 1)
+
+    # ---- algorithmic bytes of one decode-attention call (valid rows + q + out)
+    s_r = wl.sink + wl.recent
+    elt = {"f32": 4, "bf16": 2, "fp8": 1}[wl.kv_dtype]
+    row_bytes = wl.d_qk * elt + (0 if wl.v_in_k else wl.d_v * elt)
+    valid = 0
+    for L in lengths:
+        ncand = max(L - s_r, 0)
+        # rows valid while decoding: sinks+ring (full once L >= s+r) plus the kept rows
+        valid += min(L + 1, s_r) + min(ncand, wl.topk)
+    q_bytes = n * wl.n_q_heads * wl.d_qk * 2
+    o_bytes = n * wl.n_q_heads * wl.d_v * 2
+    dec_bytes = valid * row_bytes + q_bytes + o_bytes
+    dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
+    tokens = n * dsteps
+    value = tokens / (ms_step * 1e-3)
+    decode_ms_per_token_step = dec_ms * layers  # attention only, per decode step (all layers)
+
+    res = {
+        "metric": "compressed-KV decode tok/s/GPU + HBM GB/s at 128k; snap_compress latency",
+        "value": round(value, 2),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.in_dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": layers, "sequences": n, "prompt_lengths": lengths,
+                   "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
+                   "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "decode_steps": dsteps,
+                   "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
+                   "kv_dtype": wl.kv_dtype},
+        "decode_attn_ms_per_call": round(dec_ms, 4),
+        "decode_attn_hbm_gbps": round(dec_gbps, 1),
+        "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1),
+        "compress_ms_per_layer_call": round(comp_ms, 4),
+        "compress_ms_per_seq_layer": round(comp_ms / n, 4),
+        "roofline": {"bound": "hbm", "kernel": "snap_decode_attn (split-K partials + combine)",
+                     "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": dec_bytes},
+        "setup_s": round(t_setup, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, p, lengths, layers, dsteps, n, value)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value):
+    """The fp64 oracle, single-threaded on the host, on a bounded sample of the
+    same workload: one compress unit (one sequence x one KV head) at the
+    longest prompt and a few decode units (one sequence x one KV head x one
+    step), extrapolated to a whole step by unit counts."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import synth
+
+    op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
+                       p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
+    L = max(lengths)
+    q, k, v = synth.prefill(wl, 0, 0, L, device="cpu")
+    G = op.group
+    t = time.time()
+    res = oracle.compress_group(op, L, oracle.f64(q[:G]), oracle.f64(k[0]), None if v is None else oracle.f64(v[0]))
+    t_comp = time.time() - t
+    # decode units over the just-built cache
+    qd = np.random.default_rng(0).normal(size=(G, p.d_qk))
+    reps = 4
+    t = time.time()
+    for _ in range(reps):
+        oracle.decode_attn_group(op, L, len(res.sel), qd, res.cache_k, res.cache_v)
+    t_dec = (time.time() - t) / reps
+    units_comp = layers * n * p.n_kv_heads  # (scaled by each sequence's length)
+    comp_s = sum(t_comp * (Lb / L) for Lb in lengths) * layers * p.n_kv_heads
+    dec_s = t_dec * layers * n * p.n_kv_heads * dsteps
+    step_s = comp_s + dec_s
+    val = n * dsteps / step_s
+    return {"value": float(f"{val:.6g}"), "unit": "tok/s", "cores": 1, "kind": "oracle",
+            "sample": (f"1 compress unit (1 sequence x 1 KV head, L={L}) in {t_comp:.2f}s and {reps} decode units "
+                       f"(1 sequence x 1 KV head x 1 step) at {t_dec * 1e3:.1f} ms each, single thread; extrapolated "
+                       f"to {units_comp} compress units (scaled by length) and "
+                       f"{layers * n * p.n_kv_heads * dsteps} decode units per step"),
+            "gpu_over_cpu": float(f"{gpu_value / val:.4g}")}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * snapstream.h -- C ABI of the SnapStream hot path on MI355X (gfx950).
+ *
+ * SnapStream (arXiv 2511.03092) keeps, per sequence and KV head, a cache of
+ * fixed size B = sink + recent + topk rows (Sec. III-A):
+ *   rows [0, sink)                 attention-sink tokens (StreamingLLM),
+ *   rows [sink, sink+recent)       the rolling window of recent tokens, kept as
+ *                                  a ring buffer (Sec. III-B.1),
+ *   rows [sink+recent, B)          the top-K tokens chosen by SnapKV at the end
+ *                                  of prefill (Sec. III-B.2, Eq. 1-3), followed
+ *                                  by zeroed padding rows when fewer exist.
+ * The library fills that cache from a padded prefill (snap_compress), writes
+ * each decoded token into its ring row (snap_cache_append, Sec. III-C), and
+ * runs decode attention over the valid rows (snap_decode_attn).
+ *
+ * Conventions shared by every call
+ *  - Token positions are 0-based; a prompt of length L holds tokens 0..L-1 and
+ *    the first decoded token is at position L.
+ *  - Every pointer argument named as a tensor is DEVICE memory owned by the
+ *    caller.  The library allocates nothing, frees nothing and never
+ *    synchronises; all work is enqueued on `stream` (a hipStream_t, NULL = the
+ *    null stream) and the call returns once it is launched.
+ *  - Arguments are validated on the host before anything is launched; a
+ *    failure returns a non-zero snap_status, launches nothing and leaves a
+ *    message for snap_last_error().  A failed launch returns SNAP_ERR_HIP.
+ *  - Per-sequence lengths and positions are device data, so a decode step
+ *    needs no host round trip.  Device data out of range is handled without
+ *    faulting: lengths are clamped to [0, max_len]; a slot id outside
+ *    [0, n_slots) makes the call skip that sequence.
+ *  - Inputs must not alias the cache.  Calls on disjoint buffers may run
+ *    concurrently on different streams.
+ */
+#ifndef SNAPSTREAM_H
+#define SNAPSTREAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SNAP_OK = 0,
+  SNAP_ERR_INVALID_ARG = 1, /* a parameter, pointer or size is invalid     */
+  SNAP_ERR_UNSUPPORTED = 2, /* valid, but no kernel for this combination   */
+  SNAP_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than the query    */
+  SNAP_ERR_HIP = 4          /* the HIP runtime reported an error on launch */
+} snap_status;
+
+typedef enum {
+  SNAP_F32 = 0,
+  SNAP_BF16 = 1,
+  SNAP_FP8_E4M3 = 2 /* OCP E4M3 (fn): bias 7, max 448, no inf; cache only */
+} snap_dtype;
+
+typedef enum {
+  SNAP_POOL_MAX = 0, /* max pooling of the summed attention            */
+  SNAP_POOL_AVG = 1  /* average pooling (Eq. 2), zero padding, / kernel */
+} snap_pool;
+
+typedef enum {
+  SNAP_NORM_CAND = 0, /* softmax over the eviction candidates only (Eq. 3) */
+  SNAP_NORM_ROW = 1   /* softmax over the whole causal row [0, i]          */
+} snap_norm;
+
+/* The method's hyper-parameters (Sec. III, Table 6's names). */
+typedef struct {
+  int32_t n_q_heads;   /* query heads; a multiple of n_kv_heads                 */
+  int32_t n_kv_heads;  /* KV heads (1 for a shared latent cache)                */
+  int32_t d_qk;        /* query/key width: 64, 128 or 576                        */
+  int32_t d_v;         /* value width: 64, 128 or 512                            */
+  int32_t v_in_k;      /* 1: latent cache (Sec. VI) -- one stored row per token
+                          of width d_qk whose first d_v dims are the value; there
+                          is no separate V input or V cache                       */
+  int32_t sink;        /* L_sink >= 0                                            */
+  int32_t recent;      /* L_recent >= 1 (ring length)                            */
+  int32_t topk;        /* K >= 0                                                 */
+  int32_t obs_window;  /* L_obs >= 1: queries of the last L_obs prompt tokens    */
+  int32_t pool_kernel; /* odd, 1..63                                             */
+  int32_t pool;        /* snap_pool                                              */
+  int32_t norm;        /* snap_norm                                              */
+  int32_t in_dtype;    /* q / k / v inputs: SNAP_F32 or SNAP_BF16                */
+  int32_t kv_dtype;    /* cache storage: SNAP_F32, SNAP_BF16 (in_dtype == the
+                          same) or SNAP_FP8_E4M3 (with SNAP_BF16 inputs)          */
+  float sm_scale;      /* softmax scale; <= 0 means 1/sqrt(d_qk)                 */
+} snap_params;
+
+/* One layer's compressed cache (device memory, caller-owned, row-major):
+ *   k       [n_slots][n_kv_heads][B][d_qk]  kv_dtype
+ *   v       [n_slots][n_kv_heads][B][d_v]   kv_dtype; NULL when v_in_k
+ *   k_scale [n_slots][n_kv_heads] fp32      FP8 only: stored code * scale is
+ *   v_scale [n_slots][n_kv_heads] fp32      the value; set by the caller before
+ *                                           compress/append; NULL otherwise. */
+typedef struct {
+  void* k;
+  void* v;
+  float* k_scale;
+  float* v_scale;
+  int32_t n_slots;
+} snap_cache;
+
+/* Slot metadata, shared by every layer (device int32[n_slots], caller-owned):
+ *   pos[slot]    position of the token being decoded (L right after compress)
+ *   n_topk[slot] real rows in the top-K region, min(max(L-sink-recent,0), K) */
+
+/* Bytes of workspace snap_compress needs for n_seq sequences padded to
+ * max_len.  0 on invalid parameters. */
+size_t snap_compress_workspace(const snap_params* p, int32_t n_seq, int32_t max_len);
+
+/* Bytes of workspace snap_decode_attn needs for n sequences.  0 on invalid
+ * parameters. */
+size_t snap_decode_workspace(const snap_params* p, int32_t n);
+
+/* Compression at the end of prefill (Sec. III-B; Eq. 1-3).  For every
+ * sequence b and KV head g:
+ *   1. window scores: the G = n_q_heads/n_kv_heads query heads of group g at
+ *      the last w_e = min(obs_window, L) positions score every key of the
+ *      normaliser domain; softmax with sm_scale (Eq. 3);
+ *   2. the softmax weights on the candidates C = [sink, L-recent) are summed
+ *      over the window rows and the group's heads (Eq. 1);
+ *   3. 1-D pooling (stride 1, pad pool_kernel/2) over C (Eq. 2);
+ *   4. the min(K, |C|) candidates with the largest pooled score are kept (ties
+ *      to the lower token index), in ascending token order;
+ *   5. the cache of slot slot_ids[b] is rewritten: sinks, the last `recent`
+ *      tokens at their ring rows (token t at row t < sink ? t :
+ *      sink + (t - sink) mod recent), the kept tokens at rows sink+recent+m,
+ *      zeros elsewhere (fp8: quantised with the slot/head scale), and
+ *      pos[slot] = L, n_topk[slot] = min(K, |C|).
+ * Arguments (device unless noted):
+ *   slot_ids [n_seq] int32, lengths [n_seq] int32 (prompt lengths L),
+ *   max_len (host) padded length of the inputs,
+ *   q_obs [n_seq][n_q_heads][obs_window][d_qk] in_dtype; row obs_window-1 is
+ *         position L-1 (rows before position 0 are ignored),
+ *   k     [n_seq][n_kv_heads][max_len][d_qk] in_dtype (rows >= L never read),
+ *   v     [n_seq][n_kv_heads][max_len][d_v]  in_dtype, NULL when v_in_k,
+ *   sel_out    optional [n_seq][n_kv_heads][topk] int32: kept token indices,
+ *              ascending, -1 padded (NULL to skip),
+ *   pooled_out optional [n_seq][n_kv_heads][max_len] fp32: the pooled score of
+ *              every candidate at its token index, NaN elsewhere (debug),
+ *   workspace  >= snap_compress_workspace(p, n_seq, max_len) bytes, 256-byte
+ *              aligned; its contents on entry do not matter.
+ * n_seq == 0 is a no-op.  The sequences must target distinct slots. */
+snap_status snap_compress(const snap_params* p, const snap_cache* cache, int32_t* pos,
+                          int32_t* n_topk, int32_t n_seq, const int32_t* slot_ids,
+                          const int32_t* lengths, int32_t max_len, const void* q_obs,
+                          const void* k, const void* v, int32_t* sel_out, float* pooled_out,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/* Decode KV update (Sec. III-C): for each of the n sequences, the new token's
+ * keys/values k_new [n][n_kv_heads][d_qk] and v_new [n][n_kv_heads][d_v]
+ * (in_dtype; v_new NULL when v_in_k) are written to row
+ * slot_of(pos[slot]) = pos < sink ? pos : sink + (pos - sink) mod recent,
+ * which for pos >= sink is the paper's (pos - sink + recent) mod recent + sink.
+ * Sequences with pos[slot] < 0 are skipped. */
+snap_status snap_cache_append(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                              int32_t n, const int32_t* slot_ids, const void* k_new,
+                              const void* v_new, void* stream);
+
+/* Decode attention over the compressed cache (Sec. III-C; padding rows masked
+ * per Sec. III-B.2).  For sequence b with p = pos[slot] (the token already
+ * appended) the valid rows are [0, min(p+1, sink+recent)) and
+ * [sink+recent, sink+recent+n_topk[slot]); each query head h attends its KV
+ * head h / G: out[b][h] = sum_j softmax_j(sm_scale q.k_j) v_j.
+ *   q   [n][n_q_heads][d_qk] in_dtype,
+ *   out [n][n_q_heads][d_v]  out_dtype (SNAP_F32 or SNAP_BF16, rounded to
+ *                            nearest even),
+ *   workspace >= snap_decode_workspace(p, n) bytes, 256-byte aligned.
+ * Rows outside the valid set are never read. */
+snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                             const int32_t* n_topk, int32_t n, const int32_t* slot_ids,
+                             const void* q, void* out, int32_t out_dtype, void* workspace,
+                             size_t ws_bytes, void* stream);
+
+/* pos[slot_ids[b]] += 1 for b < n (once per decode step, after every layer).
+ * pos is device int32[n_slots]; slot ids outside [0, n_slots) are skipped. */
+snap_status snap_advance(int32_t* pos, int32_t n_slots, int32_t n, const int32_t* slot_ids,
+                         void* stream);
+
+/* Static description of a status code. */
+const char* snap_status_str(snap_status s);
+
+/* Message describing the most recent failure on the calling thread ("" if
+ * none).  The pointer stays valid until the thread's next library call. */
+const char* snap_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SNAPSTREAM_H */

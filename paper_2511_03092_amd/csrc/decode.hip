@@ -1,0 +1,661 @@
+// decode.hip -- decoding over the SnapStream cache (arXiv 2511.03092,
+// Sec. III-C): the in-place ring update at row L_rb, and split-K attention
+// over the valid rows (sinks + ring rows filled so far + the real top-K rows;
+// padding rows are never read, Sec. III-B.2).
+//
+//   append        one workgroup per sequence writes k/v of token pos to its row
+//   decode_mfma   per (chunk, sequence, KV head), one wave: bf16 MFMA
+//                 K x q^T for the G heads of the group (padded to 16 columns),
+//                 online softmax in the exp2 domain, MFMA V^T x P^T; bf16 or
+//                 fp8 E4M3 rows (converted to bf16 in registers)
+//   decode_generic one wave per (chunk, sequence, query head); any dtype
+//   combine       log-sum-exp merge of the chunk partials -> out
+#include <math.h>
+
+#include "snap_internal.h"
+
+namespace snap {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct DecodeArgs {
+  const void* q;         // [n][Hq][dk] (bf16 or fp32)
+  const void* ck;        // [n_slots][Hkv][B][dk]
+  const void* cv;        // [n_slots][Hkv][B][dv] or NULL (values = first dv dims of ck)
+  const float* k_scale;  // fp8 only
+  const float* v_scale;
+  const int32_t* pos;
+  const int32_t* n_topk;
+  const int32_t* slot_ids;
+  float* part;           // [n][Hq][n_chunks][dv]
+  float2* ml;            // [n][Hq][n_chunks]  (max in log2 units, sum)
+  int Hq, Hkv, G, dk, dv, sink, recent, topk, n_slots, n_chunks, q_f32;
+  float scale;
+};
+
+struct RowSpan {
+  int n1, v0, v1;
+};
+
+// Virtual row v in [0, n1 + n_topk) -> cache row: the first n1 are sinks and
+// ring rows [0, n1), the rest the real top-K rows.
+__device__ __forceinline__ int virt_row(int v, int n1, int sr) { return v < n1 ? v : sr + (v - n1); }
+
+__device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, int& slot, RowSpan& sp) {
+  slot = a.slot_ids[b];
+  if (slot < 0 || slot >= a.n_slots) return false;
+  const int sr = a.sink + a.recent;
+  const int p = a.pos[slot];
+  int nt = a.n_topk[slot];
+  nt = nt < 0 ? 0 : (nt > a.topk ? a.topk : nt);
+  const int n1 = p < 0 ? 0 : (p >= sr ? sr : p + 1);
+  const int nv = n1 + nt;
+  int cs = (nv + a.n_chunks - 1) / a.n_chunks;
+  cs = (cs + 31) & ~31;
+  sp.n1 = n1;
+  sp.v0 = chunk * cs;
+  sp.v1 = min(sp.v0 + cs, nv);
+  return true;
+}
+
+// ---------------------------------------------------------------- fp8 -> bf16
+// 8 E4M3 codes -> 8 bf16 (exact: every E4M3 value is a bf16 value).  The
+// hardware conversion gives fp32; the bf16 is its upper half.
+__device__ __forceinline__ u32x4 e4m3x8_to_bf16x8(u32x2 c) {
+  u32x4 o;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(c[h], false);
+    auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(c[h], true);
+    o[2 * h] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
+    o[2 * h + 1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+  }
+  return o;
+}
+
+template <bool FP8>
+__device__ __forceinline__ u32x4 load8(const void* base, size_t elem) {
+  if constexpr (FP8) {
+    return e4m3x8_to_bf16x8(*(const u32x2*)((const uint8_t*)base + elem));
+  } else {
+    return *(const u32x4*)((const uint16_t*)base + elem);
+  }
+}
+
+// ---------------------------------------------------------------- MFMA decode
+// KSTEPS = dk / 32, VPASS = dv / 128.  Lane l owns head l%16 of the group and,
+// per 16-row set, the output rows 4*(l/16)+e; P never leaves the lane between
+// the two products because the V operand is loaded in the matching row order.
+template <int KSTEPS, int VPASS, bool FP8>
+__global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
+  constexpr int D = KSTEPS * 32;
+  const int lane = threadIdx.x, l16 = lane & 15, lg = lane >> 4;
+  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
+  int slot;
+  RowSpan sp;
+  if (!span_of(a, b, chunk, slot, sp)) return;
+  const int sr = a.sink + a.recent;
+  const int B = sr + a.topk;
+  const int h = l16;
+  const bool hval = h < a.G;
+  const int qh = g * a.G + (hval ? h : 0);
+
+  bf16x8 qf[KSTEPS];
+  {
+    const uint16_t* qp = (const uint16_t*)a.q + ((size_t)b * a.Hq + qh) * D;
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (hval) v = *(const u32x4*)(qp + 8 * (KSTEPS * lg + t));
+      qf[t] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const size_t row0 = ((size_t)slot * a.Hkv + g) * (size_t)B;
+  const float ksc = FP8 ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
+  const float vsc = FP8 ? (a.cv ? a.v_scale : a.k_scale)[(size_t)slot * a.Hkv + g] : 1.f;
+  const float xs = a.scale * kLog2e * ksc;
+  const void* vbase = a.cv ? a.cv : a.ck;
+  const int vstride = a.cv ? a.dv : a.dk;
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 acc[VPASS][8];
+#pragma unroll
+  for (int pp = 0; pp < VPASS; ++pp)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[pp][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int vb = sp.v0; vb < sp.v1; vb += 32) {
+    // ---- loads: two 16-row K sets, eight V rows per lane
+    u32x4 ka[KSTEPS], kb[KSTEPS];
+    {
+      const int va = vb + l16, vb2 = vb + 16 + l16;
+      const bool oka = va < sp.v1, okb = vb2 < sp.v1;
+      const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
+#pragma unroll
+      for (int t = 0; t < KSTEPS; ++t) {
+        const int col = 8 * (KSTEPS * lg + t);
+        ka[t] = oka ? load8<FP8>(a.ck, ra * D + col) : u32x4{0u, 0u, 0u, 0u};
+        kb[t] = okb ? load8<FP8>(a.ck, rb * D + col) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    u32x4 vv[VPASS][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
+      const bool ok = vi < sp.v1;
+      const size_t rr = row0 + virt_row(vi, sp.n1, sr);
+#pragma unroll
+      for (int pp = 0; pp < VPASS; ++pp)
+        vv[pp][i] = ok ? load8<FP8>(vbase, rr * vstride + 128 * pp + 8 * l16) : u32x4{0u, 0u, 0u, 0u};
+    }
+    // ---- S^T = K q^T for 32 rows
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[t]), qf[t], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[t]), qf[t], s1, 0, 0, 0);
+    }
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
+      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+    }
+    float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float mn = fmaxf(m, bm);
+    float alpha = 1.f, pe[8];
+    if (mn == -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pe[i] = 0.f;
+    } else {
+      alpha = exp2f(m - mn);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pe[i] = exp2f(x[i] - mn);
+    }
+    m = mn;
+    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    u32x4 pw;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int pp = 0; pp < VPASS; ++pp)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const int u = c >> 1;
+        const uint32_t selb = (c & 1) ? 0x07060302u : 0x05040100u;
+        u32x4 av;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vv[pp][2 * i + 1][u], vv[pp][2 * i][u], selb);
+        acc[pp][c] *= alpha;
+        acc[pp][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[pp][c], 0, 0, 0);
+      }
+  }
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (!hval) return;
+  const size_t pi = ((size_t)b * a.Hq + qh) * a.n_chunks + chunk;
+  if (lg == 0) a.ml[pi] = make_float2(m, lsum);
+  float* dst = a.part + pi * a.dv;
+#pragma unroll
+  for (int pp = 0; pp < VPASS; ++pp)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float4 lo = make_float4(acc[pp][0][e], acc[pp][1][e], acc[pp][2][e], acc[pp][3][e]);
+      float4 hi = make_float4(acc[pp][4][e], acc[pp][5][e], acc[pp][6][e], acc[pp][7][e]);
+      lo.x *= vsc; lo.y *= vsc; lo.z *= vsc; lo.w *= vsc;
+      hi.x *= vsc; hi.y *= vsc; hi.z *= vsc; hi.w *= vsc;
+      float* d = dst + 128 * pp + 8 * (4 * lg + e);
+      *(float4*)d = lo;
+      *(float4*)(d + 4) = hi;
+    }
+}
+
+// ---------------------------------------------------------------- latent (MLA) decode
+// One workgroup of 4 waves per (chunk, sequence) of a shared 576-wide latent
+// cache (values = first 512 dims).  Per block of 32 rows, wave w computes the
+// partial logits over its share of the 18 k-steps of 32 dims (5,5,4,4), the
+// four partials are summed through LDS in a fixed order (so every wave holds
+// identical logits), and wave w then runs the value product for dims
+// [128w, 128w+128).  Heads beyond G (<= 16) are zero columns.
+constexpr int kMlaKSteps = 18;
+__device__ __forceinline__ int mla_kbeg(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
+__device__ __forceinline__ int mla_kcnt(int w) { return w < 2 ? 5 : 4; }
+
+template <bool FP8>
+__global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
+  constexpr int D = kMlaKSteps * 32;  // 576
+  __shared__ f32x4 sbuf[2][4][2][64];  // [parity][wave][row set][lane]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int chunk = blockIdx.x, b = blockIdx.y;  // one KV head
+  int slot;
+  RowSpan sp;
+  if (!span_of(a, b, chunk, slot, sp)) return;
+  const int sr = a.sink + a.recent;
+  const int B = sr + a.topk;
+  const int h = l16;
+  const bool hval = h < a.G;
+  const int kb = mla_kbeg(w), kc = mla_kcnt(w);
+
+  bf16x8 qf[5];
+  {
+    const uint16_t* qp = (const uint16_t*)a.q + ((size_t)b * a.Hq + (hval ? h : 0)) * D;
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (hval && t < kc) v = *(const u32x4*)(qp + 32 * kb + 8 * (kc * lg + t));
+      qf[t] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const size_t row0 = (size_t)slot * B;
+  const float ksc = FP8 ? a.k_scale[slot] : 1.f;
+  const float xs = a.scale * kLog2e * ksc;
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  int parity = 0;
+  for (int vb = sp.v0; vb < sp.v1; vb += 32, parity ^= 1) {
+    u32x4 ka[5], kbv[5];
+    {
+      const int va = vb + l16, vb2 = vb + 16 + l16;
+      const bool oka = va < sp.v1, okb = vb2 < sp.v1;
+      const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
+#pragma unroll
+      for (int t = 0; t < 5; ++t) {
+        const int col = 32 * kb + 8 * (kc * lg + t);
+        const bool tin = t < kc;
+        ka[t] = (oka && tin) ? load8<FP8>(a.ck, ra * D + col) : u32x4{0u, 0u, 0u, 0u};
+        kbv[t] = (okb && tin) ? load8<FP8>(a.ck, rb * D + col) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    u32x4 vv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
+      const size_t rr = row0 + virt_row(vi, sp.n1, sr);
+      vv[i] = vi < sp.v1 ? load8<FP8>(a.ck, rr * D + 128 * w + 8 * l16) : u32x4{0u, 0u, 0u, 0u};
+    }
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      if (t < kc) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[t]), qf[t], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kbv[t]), qf[t], s1, 0, 0, 0);
+      }
+    }
+    sbuf[parity][w][0][lane] = s0;
+    sbuf[parity][w][1][lane] = s1;
+    __syncthreads();
+    s0 = ((sbuf[parity][0][0][lane] + sbuf[parity][1][0][lane]) + sbuf[parity][2][0][lane]) + sbuf[parity][3][0][lane];
+    s1 = ((sbuf[parity][0][1][lane] + sbuf[parity][1][1][lane]) + sbuf[parity][2][1][lane]) + sbuf[parity][3][1][lane];
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
+      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+    }
+    float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float mn = fmaxf(m, bm);
+    float alpha = 1.f, pe[8];
+    if (mn == -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pe[i] = 0.f;
+    } else {
+      alpha = exp2f(m - mn);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pe[i] = exp2f(x[i] - mn);
+    }
+    m = mn;
+    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    u32x4 pw;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int u = c >> 1;
+      const uint32_t selb = (c & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 av;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vv[2 * i + 1][u], vv[2 * i][u], selb);
+      acc[c] *= alpha;
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[c], 0, 0, 0);
+    }
+  }
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (!hval) return;
+  const size_t pi = ((size_t)b * a.Hq + h) * a.n_chunks + chunk;
+  if (w == 0 && lg == 0) a.ml[pi] = make_float2(m, lsum);
+  const float vsc = FP8 ? a.k_scale[slot] : 1.f;
+  float* dst = a.part + pi * a.dv + 128 * w;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float4 lo = make_float4(acc[0][e], acc[1][e], acc[2][e], acc[3][e]);
+    float4 hi = make_float4(acc[4][e], acc[5][e], acc[6][e], acc[7][e]);
+    lo.x *= vsc; lo.y *= vsc; lo.z *= vsc; lo.w *= vsc;
+    hi.x *= vsc; hi.y *= vsc; hi.z *= vsc; hi.w *= vsc;
+    float* d = dst + 8 * (4 * lg + e);
+    *(float4*)d = lo;
+    *(float4*)(d + 4) = hi;
+  }
+}
+
+// ---------------------------------------------------------------- generic decode
+template <typename KV>
+__device__ __forceinline__ float load_kv(const void* base, size_t i, float scale) {
+  if constexpr (sizeof(KV) == 4) return ((const float*)base)[i];
+  else if constexpr (sizeof(KV) == 2) return bf16_bits_to_f32(((const uint16_t*)base)[i]);
+  else return e4m3_to_f32(((const uint8_t*)base)[i]) * scale;
+}
+
+// One wave per (chunk, sequence, query head); lane owns dims lane + 64*i.
+template <typename KV>
+__global__ __launch_bounds__(64) void decode_generic(DecodeArgs a) {
+  constexpr int kMaxDk = 9, kMaxDv = 8;  // dk <= 576, dv <= 512
+  const int lane = threadIdx.x;
+  const int chunk = blockIdx.x, bh = blockIdx.y, b = bh / a.Hq, qh = bh % a.Hq, g = qh / a.G;
+  int slot;
+  RowSpan sp;
+  if (!span_of(a, b, chunk, slot, sp)) return;
+  const int sr = a.sink + a.recent, B = sr + a.topk;
+  const size_t row0 = ((size_t)slot * a.Hkv + g) * (size_t)B;
+  const float ksc = sizeof(KV) == 1 ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
+  const float vsc = sizeof(KV) == 1 ? (a.cv ? a.v_scale : a.k_scale)[(size_t)slot * a.Hkv + g] : 1.f;
+  const void* vbase = a.cv ? a.cv : a.ck;
+  const int vstride = a.cv ? a.dv : a.dk;
+  float qv[kMaxDk];
+#pragma unroll
+  for (int i = 0; i < kMaxDk; ++i) {
+    int d = lane + 64 * i;
+    float x = 0.f;
+    if (d < a.dk) {
+      size_t qi = ((size_t)b * a.Hq + qh) * a.dk + d;
+      x = a.q_f32 ? ((const float*)a.q)[qi] : bf16_bits_to_f32(((const uint16_t*)a.q)[qi]);
+    }
+    qv[i] = x;
+  }
+  float acc[kMaxDv];
+#pragma unroll
+  for (int i = 0; i < kMaxDv; ++i) acc[i] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+  const float xs = a.scale * kLog2e;
+  for (int v = sp.v0; v < sp.v1; ++v) {
+    const size_t row = row0 + virt_row(v, sp.n1, sr);
+    float dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxDk; ++i) {
+      int d = lane + 64 * i;
+      if (d < a.dk) dot = fmaf(qv[i], load_kv<KV>(a.ck, row * a.dk + d, ksc), dot);
+    }
+    dot = warp_sum(dot);
+    const float x = dot * xs;
+    const float mn = fmaxf(m, x);
+    const float alpha = exp2f(m - mn);
+    const float pe = exp2f(x - mn);
+    lsum = lsum * alpha + pe;
+    m = mn;
+#pragma unroll
+    for (int i = 0; i < kMaxDv; ++i) {
+      int d = lane + 64 * i;
+      float vx = d < a.dv ? load_kv<KV>(vbase, row * vstride + d, vsc) : 0.f;
+      acc[i] = fmaf(pe, vx, acc[i] * alpha);
+    }
+  }
+  const size_t pi = ((size_t)b * a.Hq + qh) * a.n_chunks + chunk;
+  if (lane == 0) a.ml[pi] = make_float2(m, lsum);
+  float* dst = a.part + pi * a.dv;
+#pragma unroll
+  for (int i = 0; i < kMaxDv; ++i) {
+    int d = lane + 64 * i;
+    if (d < a.dv) dst[d] = acc[i];
+  }
+}
+
+// ---------------------------------------------------------------- combine
+struct CombineArgs {
+  const float* part;
+  const float2* ml;
+  const int32_t* slot_ids;
+  void* out;  // [n][Hq][dv]
+  int Hq, dv, n_chunks, n_slots, out_bf16;
+};
+
+__global__ __launch_bounds__(256) void combine(CombineArgs a) {
+  const int bh = blockIdx.x, b = bh / a.Hq;
+  const int slot = a.slot_ids[b];
+  if (slot < 0 || slot >= a.n_slots) return;
+  const float2* ml = a.ml + (size_t)bh * a.n_chunks;
+  float M = -INFINITY;
+  for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, ml[c].x);
+  float wsum = 0.f;
+  for (int c = 0; c < a.n_chunks; ++c) {
+    float2 v = ml[c];
+    if (v.x != -INFINITY) wsum += exp2f(v.x - M) * v.y;
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const float* part = a.part + (size_t)bh * a.n_chunks * a.dv;
+  for (int d = threadIdx.x; d < a.dv; d += blockDim.x) {
+    float o = 0.f;
+    for (int c = 0; c < a.n_chunks; ++c) {
+      float mc = ml[c].x;
+      if (mc != -INFINITY) o = fmaf(exp2f(mc - M), part[(size_t)c * a.dv + d], o);
+    }
+    o *= inv;
+    size_t oi = (size_t)bh * a.dv + d;
+    if (a.out_bf16)
+      ((uint16_t*)a.out)[oi] = (uint16_t)f32_to_bf16_bits(o);
+    else
+      ((float*)a.out)[oi] = o;
+  }
+}
+
+// ---------------------------------------------------------------- append / advance
+struct AppendArgs {
+  const void* k_new;  // [n][Hkv][dk]
+  const void* v_new;  // [n][Hkv][dv] or NULL
+  void* ck;
+  void* cv;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* pos;
+  const int32_t* slot_ids;
+  int Hkv, dk, dv, sink, recent, topk, n_slots;
+};
+
+template <typename In, typename Out>
+__device__ __forceinline__ void put8(const In* src, Out* dst, float scale) {
+  if constexpr (sizeof(Out) == 1) {
+    float f[8];
+    if constexpr (sizeof(In) == 2) {
+      u32x4 raw = *(const u32x4*)src;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = bf16_bits_to_f32(raw[i] & 0xffffu);
+        f[2 * i + 1] = bf16_bits_to_f32(raw[i] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) f[i] = ((const float*)src)[i];
+    }
+    u32x2 o;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(f[h2 * 4 + i] / scale) << (8 * i);
+      o[h2] = w;
+    }
+    *(u32x2*)dst = o;
+  } else if constexpr (sizeof(In) == 2) {
+    *(u32x4*)dst = *(const u32x4*)src;
+  } else {
+    *(u32x4*)dst = *(const u32x4*)src;
+    *(u32x4*)((float*)dst + 4) = *(const u32x4*)((const float*)src + 4);
+  }
+}
+
+template <typename In, typename Out>
+__global__ __launch_bounds__(256) void append(AppendArgs a) {
+  const int b = blockIdx.x;
+  const int slot = a.slot_ids[b];
+  if (slot < 0 || slot >= a.n_slots) return;
+  const int p = a.pos[slot];
+  if (p < 0) return;
+  const int s = a.sink, r = a.recent, B = s + r + a.topk;
+  const int row = p < s ? p : s + (p - s) % r;
+  const int kc = a.dk / 8, vc = a.v_new ? a.dv / 8 : 0;
+  for (int i = threadIdx.x; i < a.Hkv * (kc + vc); i += blockDim.x) {
+    const int g = i / (kc + vc), c = i % (kc + vc);
+    const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + row;
+    if (c < kc) {
+      const float sc = sizeof(Out) == 1 ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
+      put8<In, Out>((const In*)a.k_new + ((size_t)b * a.Hkv + g) * a.dk + 8 * c,
+                    (Out*)a.ck + crow * a.dk + 8 * c, sc);
+    } else {
+      const int cc = c - kc;
+      const float sc = sizeof(Out) == 1 ? a.v_scale[(size_t)slot * a.Hkv + g] : 1.f;
+      put8<In, Out>((const In*)a.v_new + ((size_t)b * a.Hkv + g) * a.dv + 8 * cc,
+                    (Out*)a.cv + crow * a.dv + 8 * cc, sc);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids) {
+  for (int b = threadIdx.x + blockIdx.x * blockDim.x; b < n; b += blockDim.x * gridDim.x) {
+    int s = slot_ids[b];
+    if (s >= 0 && s < n_slots) atomicAdd(&pos[s], 1);
+  }
+}
+
+// ---------------------------------------------------------------- host side
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Geometry decode_geometry(const snap_params& p, int n) {
+  Geometry g{};
+  const int B = p.sink + p.recent + p.topk;
+  const int units = (n > 0 ? n : 1) * p.n_kv_heads;
+  int want = (2048 + units - 1) / units;
+  int maxc = (B + 63) / 64;
+  if (maxc < 1) maxc = 1;
+  g.n_chunks = want < 1 ? 1 : (want > maxc ? maxc : want);
+  size_t off = 0;
+  g.off_part = off;
+  off = align256(off + (size_t)(n > 0 ? n : 1) * p.n_q_heads * g.n_chunks * p.d_v * sizeof(float));
+  g.off_ml = off;
+  off = align256(off + (size_t)(n > 0 ? n : 1) * p.n_q_heads * g.n_chunks * sizeof(float2));
+  g.decode_bytes = off;
+  return g;
+}
+
+snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32_t* pos, const int32_t* n_topk,
+                          int n, const int32_t* slot_ids, const void* q, void* out, int out_dtype, void* ws,
+                          hipStream_t stream) {
+  Geometry geo = decode_geometry(p, n);
+  DecodeArgs a;
+  a.q = q;
+  a.ck = c.k;
+  a.cv = p.v_in_k ? nullptr : c.v;
+  a.k_scale = c.k_scale;
+  a.v_scale = c.v_scale;
+  a.pos = pos;
+  a.n_topk = n_topk;
+  a.slot_ids = slot_ids;
+  a.part = (float*)((unsigned char*)ws + geo.off_part);
+  a.ml = (float2*)((unsigned char*)ws + geo.off_ml);
+  a.Hq = p.n_q_heads;
+  a.Hkv = p.n_kv_heads;
+  a.G = p.n_q_heads / p.n_kv_heads;
+  a.dk = p.d_qk;
+  a.dv = p.d_v;
+  a.sink = p.sink;
+  a.recent = p.recent;
+  a.topk = p.topk;
+  a.n_slots = c.n_slots;
+  a.n_chunks = geo.n_chunks;
+  a.q_f32 = p.in_dtype == SNAP_F32;
+  a.scale = p.sm_scale > 0.f ? p.sm_scale : 1.0f / sqrtf((float)p.d_qk);
+
+  const bool mfma_ok = p.in_dtype == SNAP_BF16 && !p.v_in_k && p.d_qk == 128 && p.d_v == 128 &&
+                       (p.kv_dtype == SNAP_BF16 || p.kv_dtype == SNAP_FP8_E4M3);
+  const bool mla_ok = p.in_dtype == SNAP_BF16 && p.v_in_k && p.n_kv_heads == 1 && p.d_qk == 576 && p.d_v == 512 &&
+                      (p.kv_dtype == SNAP_BF16 || p.kv_dtype == SNAP_FP8_E4M3);
+  if (mla_ok) {
+    dim3 grid(geo.n_chunks, n);
+    if (p.kv_dtype == SNAP_FP8_E4M3)
+      hipLaunchKernelGGL((decode_mla<true>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_mla<false>), grid, dim3(256), 0, stream, a);
+  } else if (mfma_ok) {
+    dim3 grid(geo.n_chunks, n * p.n_kv_heads);
+    if (p.kv_dtype == SNAP_FP8_E4M3)
+      hipLaunchKernelGGL((decode_mfma<4, 1, true>), grid, dim3(64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_mfma<4, 1, false>), grid, dim3(64), 0, stream, a);
+  } else {
+    dim3 grid(geo.n_chunks, n * p.n_q_heads);
+    if (p.kv_dtype == SNAP_F32)
+      hipLaunchKernelGGL((decode_generic<float>), grid, dim3(64), 0, stream, a);
+    else if (p.kv_dtype == SNAP_BF16)
+      hipLaunchKernelGGL((decode_generic<uint16_t>), grid, dim3(64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_generic<uint8_t>), grid, dim3(64), 0, stream, a);
+  }
+  if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+  CombineArgs ca;
+  ca.part = a.part;
+  ca.ml = a.ml;
+  ca.slot_ids = slot_ids;
+  ca.out = out;
+  ca.Hq = p.n_q_heads;
+  ca.dv = p.d_v;
+  ca.n_chunks = geo.n_chunks;
+  ca.n_slots = c.n_slots;
+  ca.out_bf16 = out_dtype == SNAP_BF16;
+  hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads), dim3(128), 0, stream, ca);
+  if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+  return SNAP_OK;
+}
+
+snap_status launch_append(const snap_params& p, const snap_cache& c, const int32_t* pos, int n,
+                          const int32_t* slot_ids, const void* k_new, const void* v_new, hipStream_t stream) {
+  AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = p.v_in_k ? nullptr : v_new;
+  a.ck = c.k;
+  a.cv = p.v_in_k ? nullptr : c.v;
+  a.k_scale = c.k_scale;
+  a.v_scale = c.v_scale;
+  a.pos = pos;
+  a.slot_ids = slot_ids;
+  a.Hkv = p.n_kv_heads;
+  a.dk = p.d_qk;
+  a.dv = p.d_v;
+  a.sink = p.sink;
+  a.recent = p.recent;
+  a.topk = p.topk;
+  a.n_slots = c.n_slots;
+  if (p.kv_dtype == SNAP_FP8_E4M3)
+    hipLaunchKernelGGL((append<uint16_t, uint8_t>), dim3(n), dim3(256), 0, stream, a);
+  else if (p.kv_dtype == SNAP_BF16)
+    hipLaunchKernelGGL((append<uint16_t, uint16_t>), dim3(n), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((append<float, float>), dim3(n), dim3(256), 0, stream, a);
+  return hipGetLastError() == hipSuccess ? SNAP_OK : SNAP_ERR_HIP;
+}
+
+snap_status launch_advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids, hipStream_t stream) {
+  hipLaunchKernelGGL(advance, dim3(1), dim3(256), 0, stream, pos, n_slots, n, slot_ids);
+  return hipGetLastError() == hipSuccess ? SNAP_OK : SNAP_ERR_HIP;
+}
+
+}  // namespace snap

@@ -1,0 +1,112 @@
+// snap_internal.h -- device helpers and the launcher interface shared by the
+// HIP translation units of libsnapstream.  gfx950 (CDNA4) only: 64-lane
+// wavefronts, bf16 MFMA 16x16x32, OCP fp8.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "snapstream.h"
+
+namespace snap {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- numerics
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// fp32 -> OCP E4M3 code: round to nearest even, saturate at +-448, NaN -> 0x7F.
+__device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
+  uint32_t u = __float_as_uint(v);
+  uint32_t sign = (u >> 24) & 0x80u;
+  uint32_t a = u & 0x7fffffffu;
+  if (a > 0x7f800000u) return 0x7fu;
+  if (a >= 0x43e00000u) return sign | 0x7eu;  // |v| >= 448
+  if (a >= 0x3c800000u) {                       // |v| >= 2^-6: normal code
+    uint32_t r = a + 0x7ffffu + ((a >> 20) & 1u);
+    uint32_t e = (r >> 23) - 120u;
+    uint32_t m = (r >> 20) & 7u;
+    return sign | (e << 3) | m;
+  }
+  // subnormal codes m * 2^-9 (m = 8 is the smallest normal, code 0x08)
+  float q = __builtin_rintf(__uint_as_float(a) * 512.0f);
+  return sign | (uint32_t)q;
+}
+
+// OCP E4M3 code -> fp32 (exact).
+__device__ __forceinline__ float e4m3_to_f32(uint32_t c) {
+  uint32_t cm = c & 0x7fu;
+  float mag = (cm < 8u) ? (float)cm * (1.0f / 512.0f) : __uint_as_float((cm << 20) + (120u << 23));
+  if (cm == 0x7fu) mag = __builtin_nanf("");
+  return (c & 0x80u) ? -mag : mag;
+}
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// ---------------------------------------------------------------- launch context
+struct Geometry {
+  // compress
+  int rows;         // G * obs_window
+  int rows_pad;     // rows rounded up to 32 (one wave per 32 rows)
+  int key_chunk;    // keys per workgroup in the score passes
+  int n_kchunks;    // score-pass chunks per (sequence, KV head)
+  int n_splits;     // candidate splits per group in pool/select
+  size_t off_stats, off_rowref, off_A, off_P, off_hist, off_done, off_state, off_counts, off_sel;
+  size_t compress_bytes;
+  // decode
+  int n_chunks;     // split-K chunks per (sequence, KV head)
+  size_t off_part, off_ml;
+  size_t decode_bytes;
+};
+
+constexpr int kKeyTile = 64;      // keys staged in LDS per score-pass iteration
+constexpr int kCandChunk = 2048;  // candidates per pool/select workgroup
+constexpr int kSelThreads = 256;
+constexpr int kRadixBins = 2048;
+
+struct RadixState {
+  uint32_t prefix;  // decided high bits of the threshold
+  uint32_t mask;    // which bits are decided
+  int32_t krem;     // how many elements equal to the threshold prefix still to take
+  int32_t keff;     // how many candidates are kept in total
+  int32_t mode;     // 0: nothing kept, 1: all candidates kept, 2: radix select
+  int32_t pad[3];
+};
+
+Geometry compress_geometry(const snap_params& p, int n_seq, int max_len);
+Geometry decode_geometry(const snap_params& p, int n);
+
+snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* pos,
+                            int32_t* n_topk, int n_seq, const int32_t* slot_ids,
+                            const int32_t* lengths, int max_len, const void* q_obs, const void* k,
+                            const void* v, int32_t* sel_out, float* pooled_out, void* ws,
+                            hipStream_t stream);
+snap_status launch_append(const snap_params& p, const snap_cache& c, const int32_t* pos, int n,
+                          const int32_t* slot_ids, const void* k_new, const void* v_new,
+                          hipStream_t stream);
+snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32_t* pos,
+                          const int32_t* n_topk, int n, const int32_t* slot_ids, const void* q,
+                          void* out, int out_dtype, void* ws, hipStream_t stream);
+snap_status launch_advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids, hipStream_t stream);
+
+void set_error(const char* fmt, ...);
+
+}  // namespace snap

@@ -233,6 +233,28 @@ def decode_inputs(wl: Workload, layer: int, step: int, positions, device="cpu", 
     return cast(q, wl.in_dtype), cast(k, wl.in_dtype), None if v is None else cast(v, wl.in_dtype)
 
 
+def decode_inputs_all(wl: Workload, layer: int, steps: int, start_positions, device="cpu", salt: int = 0):
+    """Decode inputs of `steps` consecutive steps at once (one random draw per
+    tensor): q [steps][n][Hq][dqk], k [steps][n][Hkv][k_width], v or None.
+    Step t of sequence b sits at position start_positions[b] + t."""
+    n = len(start_positions)
+    sd = lambda p: seed_of(wl.cfg_id, layer, 0, p, salt * 1000003 + 777777)
+    q = _randn((steps, n, wl.n_q_heads, wl.d_qk), sd(P_DEC_Q), device)
+    k = _randn((steps, n, wl.n_kv_heads, wl.k_width), sd(P_DEC_K), device)
+    v = None if wl.v_in_k else _randn((steps, n, wl.n_kv_heads, wl.d_v), sd(P_DEC_V), device)
+    if wl.rope:
+        start = torch.as_tensor(start_positions, device=device)
+        pos = (start[None, :] + torch.arange(steps, device=device)[:, None]).reshape(-1)
+        qq = q.reshape(steps * n, wl.n_q_heads, wl.d_qk).transpose(0, 1)   # [H][steps*n][D]
+        kk = k.reshape(steps * n, wl.n_kv_heads, wl.k_width).transpose(0, 1)
+        qq = rope_(qq.contiguous(), pos, wl.rope_theta)
+        kk = rope_(kk.contiguous(), pos, wl.rope_theta)
+        q = qq.transpose(0, 1).reshape(steps, n, wl.n_q_heads, wl.d_qk)
+        k = kk.transpose(0, 1).reshape(steps, n, wl.n_kv_heads, wl.k_width)
+    return cast(q, wl.in_dtype).contiguous(), cast(k, wl.in_dtype).contiguous(), \
+        None if v is None else cast(v, wl.in_dtype).contiguous()
+
+
 def small(wl: Workload, **kw) -> Workload:
     """A copy with some fields replaced (for scaled-down test cases)."""
     return replace(wl, **kw)

@@ -1,0 +1,216 @@
+"""Helpers shared by the GPU parity tests: run the HIP path through the C ABI
+on seeded synthetic inputs and check it against the fp64 oracle.
+
+Acceptance rules (the benchmark spec's bar):
+  * kept index sets: exact, except swaps between candidates whose oracle
+    pooled scores lie within 1e-6 (relative) of the K-th largest score;
+  * cache bytes: sinks, ring rows and every kept row are exact copies of the
+    input rows (fp8: exactly the oracle's code of x / scale);
+  * decode outputs, recomputed by the oracle on the GPU's own cache bytes:
+    max-abs 1e-4 (fp32) or 2e-2 (bf16 / fp8).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2511_03092_amd as snap
+import synth
+
+SEL_RTOL = 1e-6
+TOL = {"f32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
+DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
+
+
+def params_of(wl: synth.Workload, **over) -> snap.Params:
+    kw = dict(n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, d_qk=wl.d_qk, d_v=wl.d_v, sink=wl.sink,
+              recent=wl.recent, topk=wl.topk, obs_window=wl.obs_window, pool_kernel=wl.pool_kernel,
+              pool=wl.pool, norm=wl.norm, v_in_k=wl.v_in_k, in_dtype=DT[wl.in_dtype], kv_dtype=DT[wl.kv_dtype])
+    kw.update(over)
+    return snap.Params(**kw)
+
+
+def oracle_params(p: snap.Params) -> oracle.Params:
+    return oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
+                         p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
+
+
+class GpuCache:
+    """One layer's cache on the device plus slot metadata."""
+
+    def __init__(self, p: snap.Params, n_slots: int, dev="cuda"):
+        self.p = p
+        B = p.budget
+        dt = {snap.SNAP_F32: torch.float32, snap.SNAP_BF16: torch.bfloat16, snap.SNAP_FP8_E4M3: torch.uint8}[p.kv_dtype]
+        # canary-filled: rows the library must write are checked, others must stay untouched
+        self.k = torch.full((n_slots, p.n_kv_heads, B, p.d_qk), 0, dtype=dt, device=dev)
+        self.v = None if p.v_in_k else torch.full((n_slots, p.n_kv_heads, B, p.d_v), 0, dtype=dt, device=dev)
+        self.k_scale = self.v_scale = None
+        if p.kv_dtype == snap.SNAP_FP8_E4M3:
+            self.k_scale = torch.ones((n_slots, p.n_kv_heads), dtype=torch.float32, device=dev)
+            self.v_scale = None if p.v_in_k else torch.ones((n_slots, p.n_kv_heads), dtype=torch.float32, device=dev)
+        self.pos = torch.full((n_slots,), -1, dtype=torch.int32, device=dev)
+        self.n_topk = torch.zeros((n_slots,), dtype=torch.int32, device=dev)
+        self.n_slots = n_slots
+
+    def c(self):
+        return snap.cache_struct(self.k, self.v, self.k_scale, self.v_scale)
+
+    def host_values(self):
+        """Cache values as fp64 numpy (fp8 codes dequantised exactly)."""
+        def val(t, sc):
+            if t is None:
+                return None
+            if t.dtype == torch.uint8:
+                table = torch.tensor([oracle.e4m3_value(c) for c in range(256)], dtype=torch.float64)
+                x = table[t.cpu().long()]
+                return (x * sc.cpu().double()[:, :, None, None]).numpy()
+            return t.cpu().double().numpy()
+        return val(self.k, self.k_scale), val(self.v, self.v_scale)
+
+
+def gpu_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, debug=True):
+    dev = cache.k.device
+    n_seq, max_len = k.shape[0], k.shape[2]
+    qd, kd = q.to(dev), k.to(dev)
+    vd = None if v is None else v.to(dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.tensor(slots, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_compress_workspace(p, n_seq, max_len), dev)
+    sel = torch.empty((n_seq, p.n_kv_heads, max(p.topk, 1)), dtype=torch.int32, device=dev) if debug else None
+    pooled = torch.empty((n_seq, p.n_kv_heads, max_len), dtype=torch.float32, device=dev) if debug else None
+    snap.snap_compress(p, cache.c(), cache.pos, cache.n_topk, sl, lens, qd, kd, vd, ws, sel, pooled)
+    torch.cuda.synchronize()
+    return (None if sel is None else sel.cpu().numpy()), (None if pooled is None else pooled.cpu().numpy())
+
+
+def check_selection(gsel, P, L, s, r, K, tol=SEL_RTOL):
+    """gsel: GPU output [K] (ascending, -1 pad); P: oracle pooled scores [L]."""
+    c0, c1 = s, max(L - r, s)
+    n = c1 - c0
+    keff = min(K, n)
+    S = gsel[:keff]
+    assert np.all(gsel[keff:K] == -1), "padding of sel_out"
+    assert len(np.unique(S)) == keff, "duplicates"
+    assert np.all(np.diff(S) > 0), "not ascending"
+    assert np.all((S >= c0) & (S < c1)), "outside candidates"
+    if keff == 0 or keff == n:
+        assert S.tolist() == list(range(c0, c0 + keff))
+        return 0
+    cand = np.arange(c0, c1)
+    tau = np.sort(P[c0:c1])[::-1][keff - 1]
+    dropped = np.setdiff1d(cand, S)
+    assert P[S].min() >= tau * (1 - tol), ("kept candidate below threshold", P[S].min(), tau)
+    assert P[dropped].max() <= tau * (1 + tol), ("dropped candidate above threshold", P[dropped].max(), tau)
+    ora = oracle.topk(L, s, r, K, P)
+    return int(len(np.setdiff1d(ora, S)))  # number of tolerated swaps
+
+
+def expected_cache(L, s, r, K, x, sel):
+    return oracle.assemble(L, s, r, K, x, np.asarray(sel, np.int32))
+
+
+def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gsel, gpooled):
+    """Full check of one compress call.  Returns the tolerated swaps, the max
+    relative error of the pooled scores over all candidates, and over the
+    decision band (oracle score within a factor 4 of the K-th largest): a band
+    error <= 5e-7 means no two candidates can trade places unless their exact
+    scores differ by less than 1e-6."""
+    op = oracle_params(p)
+    res = oracle.compress(op, lengths, q, k, v)
+    ck, cv = cache.host_values()
+    pos = cache.pos.cpu().numpy()
+    nt = cache.n_topk.cpu().numpy()
+    kin = oracle.f64(k)
+    vin = None if v is None else oracle.f64(v)
+    swaps, rel, band_rel = 0, 0.0, 0.0
+    for b, L in enumerate(lengths):
+        sl = slots[b]
+        if sl < 0 or sl >= cache.n_slots:
+            continue
+        assert pos[sl] == L and nt[sl] == res.n_topk[b]
+        for g in range(p.n_kv_heads):
+            gr = res.groups[b][g]
+            c0, c1 = p.sink, L - p.recent
+            if c1 > c0:
+                P = gr.P
+                gp = gpooled[b, g, c0:c1].astype(np.float64)
+                denom = np.maximum(np.abs(P[c0:c1]), 1e-30)
+                relv = np.abs(gp - P[c0:c1]) / denom
+                rel = max(rel, float(np.max(relv)))
+                keff_g = min(p.topk, c1 - c0)
+                if 0 < keff_g < c1 - c0:
+                    # decision band: candidates within a factor 4 of the K-th score
+                    tau = np.sort(P[c0:c1])[::-1][keff_g - 1]
+                    band = (P[c0:c1] >= tau / 4) & (P[c0:c1] <= tau * 4)
+                    band_rel = max(band_rel, float(np.max(relv[band])))
+                assert np.all(np.isnan(gpooled[b, g, :c0])) and np.all(np.isnan(gpooled[b, g, c1:L]))
+                swaps += check_selection(gsel[b, g], P, L, p.sink, p.recent, p.topk)
+            else:
+                assert np.all(gsel[b, g, :p.topk] == -1)
+            keff = res.n_topk[b]
+            used = gsel[b, g, :keff]
+            ek = expected_cache(L, p.sink, p.recent, p.topk, kin[b, g, :L], used)
+            if p.kv_dtype == snap.SNAP_FP8_E4M3:
+                sc = float(cache.k_scale[sl, g].item())
+                codes = oracle.quantize(ek, sc).reshape(ek.shape)
+                assert np.array_equal(cache.k[sl, g].cpu().numpy(), codes), "fp8 K codes"
+            else:
+                assert np.array_equal(ck[sl, g], ek), f"K cache rows (seq {b}, head {g})"
+            if vin is not None:
+                ev = expected_cache(L, p.sink, p.recent, p.topk, vin[b, g, :L], used)
+                if p.kv_dtype == snap.SNAP_FP8_E4M3:
+                    sc = float(cache.v_scale[sl, g].item())
+                    codes = oracle.quantize(ev, sc).reshape(ev.shape)
+                    assert np.array_equal(cache.v[sl, g].cpu().numpy(), codes), "fp8 V codes"
+                else:
+                    assert np.array_equal(cv[sl, g], ev), f"V cache rows (seq {b}, head {g})"
+    return dict(swaps=swaps, pooled_rel_err=rel, band_rel_err=band_rel, oracle=res)
+
+
+def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, steps, out_dtype, tol,
+                 check_every=1, layer=0, salt=0):
+    """Run `steps` decode steps (append, attend, advance) and check each checked
+    step against the oracle on the GPU's cache.  Returns the max abs error."""
+    dev = cache.k.device
+    sl = torch.tensor(slots, dtype=torch.int32, device=dev)
+    n = len(slots)
+    ws = snap.workspace(snap.snap_decode_workspace(p, n), dev)
+    out = torch.empty((n, p.n_q_heads, p.d_v), dtype=out_dtype, device=dev)
+    op = oracle_params(p)
+    worst = 0.0
+    for step in range(steps):
+        positions = cache.pos[sl].cpu().tolist()
+        q, kn, vn = synth.decode_inputs(wl, layer, step, positions, salt=salt)
+        check = (step % check_every == 0) or step == steps - 1
+        if check:
+            before_k, before_v = cache.host_values()
+        snap.snap_cache_append(p, cache.c(), cache.pos, sl, kn.to(dev), None if vn is None else vn.to(dev))
+        snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), out, ws)
+        snap.snap_advance(cache.pos, sl)
+        torch.cuda.synchronize()
+        if not check:
+            continue
+        ck, cv = cache.host_values()
+        nt = cache.n_topk.cpu().numpy()
+        # the append touched exactly one row per (slot, head): the ring row of the position
+        for i, s_ in enumerate(slots):
+            row = oracle.slot_of(positions[i], p.sink, p.recent)
+            mask = np.ones(ck.shape[2], bool)
+            mask[row] = False
+            assert np.array_equal(ck[s_][:, mask], before_k[s_][:, mask]), "append wrote outside its row"
+            if p.kv_dtype != snap.SNAP_FP8_E4M3:
+                assert np.array_equal(ck[s_][:, row], oracle.f64(kn[i])), "appended K row"
+                if cv is not None:
+                    assert np.array_equal(cv[s_][:, row], oracle.f64(vn[i])), "appended V row"
+            else:
+                for g in range(p.n_kv_heads):
+                    codes = oracle.quantize(oracle.f64(kn[i, g]), float(cache.k_scale[s_, g]))
+                    assert np.array_equal(cache.k[s_, g, row].cpu().numpy(), codes)
+        exp = oracle.decode_attn(op, positions, nt[slots], q, ck[slots], None if cv is None else cv[slots])
+        got = out.double().cpu().numpy()
+        err = float(np.max(np.abs(got - exp)))
+        worst = max(worst, err)
+        assert err <= tol, f"decode step {step}: max abs err {err}"
+    return worst

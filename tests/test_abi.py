@@ -1,0 +1,131 @@
+"""The C ABI loads, exports every declared symbol, and validates on the host.
+
+No compute call is made here: every call below fails host-side validation
+before anything would be launched, so these run without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2511_03092_amd as snap
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "snapstream.h")
+FAKE = 0x100000  # aligned, never dereferenced (validation fails first)
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(snap_[a-z_]+)\s*\(", src)))
+
+
+def _params(**kw):
+    base = dict(n_q_heads=32, n_kv_heads=8, d_qk=128, d_v=128, sink=4, recent=1024, topk=3068,
+                obs_window=32, pool_kernel=7)
+    base.update(kw)
+    return snap.Params(**base)
+
+
+def test_library_exports_every_declared_symbol():
+    L = snap.lib()
+    names = _declared()
+    assert set(names) == set(snap.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for s in range(5):
+        assert snap.snap_status_str(s)
+    assert snap.snap_status_str(0) == "ok"
+
+
+def test_workspace_queries_are_host_only():
+    p = _params()
+    ws = snap.snap_compress_workspace(p, 1, 32768)
+    # at least A and P over the padded length
+    assert ws >= 2 * 8 * 32768 * 4
+    assert snap.snap_compress_workspace(p, 8, 131072) > ws
+    assert snap.snap_decode_workspace(p, 8) > 0
+    assert snap.snap_compress_workspace(_params(pool_kernel=4), 1, 100) == 0
+    assert snap.snap_decode_workspace(_params(n_q_heads=30), 1) == 0
+
+
+def _compress_status(p, ws_bytes=1 << 30, **kw):
+    L = snap.lib()
+    cache = snap.SnapCache(FAKE, FAKE if not p.v_in_k else None, None, None, 4)
+    args = dict(pos=FAKE, n_topk=FAKE, n_seq=1, slot_ids=FAKE, lengths=FAKE, max_len=4096,
+                q=FAKE, k=FAKE, v=None if p.v_in_k else FAKE, ws=FAKE)
+    args.update(kw)
+    st = L.snap_compress(ctypes.byref(p.c()), ctypes.byref(cache), args["pos"], args["n_topk"], args["n_seq"],
+                         args["slot_ids"], args["lengths"], args["max_len"], args["q"], args["k"], args["v"],
+                         None, None, args["ws"], ws_bytes, None)
+    return st, L.snap_last_error().decode()
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(n_q_heads=30), snap.SNAP_ERR_INVALID_ARG),
+    (dict(recent=0), snap.SNAP_ERR_INVALID_ARG),
+    (dict(pool_kernel=6), snap.SNAP_ERR_INVALID_ARG),
+    (dict(pool_kernel=65), snap.SNAP_ERR_INVALID_ARG),
+    (dict(d_qk=96, d_v=96), snap.SNAP_ERR_UNSUPPORTED),
+    (dict(n_q_heads=64, n_kv_heads=2), snap.SNAP_ERR_UNSUPPORTED),
+    (dict(in_dtype=snap.SNAP_F32, kv_dtype=snap.SNAP_BF16), snap.SNAP_ERR_UNSUPPORTED),
+    (dict(obs_window=128), snap.SNAP_ERR_UNSUPPORTED),
+    (dict(norm=5), snap.SNAP_ERR_INVALID_ARG),
+])
+def test_invalid_params_rejected(bad, code):
+    st, msg = _compress_status(_params(**bad))
+    assert st == code and msg
+
+
+def test_workspace_too_small():
+    p = _params()
+    need = snap.snap_compress_workspace(p, 1, 4096)
+    st, msg = _compress_status(p, ws_bytes=need - 1)
+    assert st == snap.SNAP_ERR_WORKSPACE and str(need) in msg
+    st, _ = _compress_status(p, ws=FAKE + 16)  # not 256-byte aligned
+    assert st == snap.SNAP_ERR_WORKSPACE
+
+
+def test_null_and_misaligned_pointers():
+    p = _params()
+    assert _compress_status(p, k=None)[0] == snap.SNAP_ERR_INVALID_ARG
+    assert _compress_status(p, q=FAKE + 2)[0] == snap.SNAP_ERR_INVALID_ARG
+    assert _compress_status(p, lengths=None)[0] == snap.SNAP_ERR_INVALID_ARG
+    assert _compress_status(p, max_len=0)[0] == snap.SNAP_ERR_INVALID_ARG
+    lat = _params(n_q_heads=8, n_kv_heads=1, d_qk=576, d_v=512, v_in_k=True)
+    assert _compress_status(lat, v=FAKE)[0] == snap.SNAP_ERR_INVALID_ARG
+    assert _compress_status(_params(v_in_k=False, d_qk=576, d_v=512, n_q_heads=8, n_kv_heads=1))[0] == \
+        snap.SNAP_ERR_UNSUPPORTED
+
+
+def test_fp8_cache_needs_scales():
+    p = _params(kv_dtype=snap.SNAP_FP8_E4M3)
+    st, msg = _compress_status(p)
+    assert st == snap.SNAP_ERR_INVALID_ARG and "scale" in msg
+
+
+def test_empty_batch_is_a_no_op():
+    # n_seq == 0 returns before any launch
+    st, _ = _compress_status(_params(), n_seq=0)
+    assert st == snap.SNAP_OK
+
+
+def test_decode_and_append_validation():
+    L = snap.lib()
+    p = _params()
+    cache = snap.SnapCache(FAKE, FAKE, None, None, 4)
+    st = L.snap_decode_attn(ctypes.byref(p.c()), ctypes.byref(cache), FAKE, FAKE, 2, FAKE, FAKE, FAKE,
+                            snap.SNAP_BF16, FAKE, 16, None)
+    assert st == snap.SNAP_ERR_WORKSPACE
+    st = L.snap_decode_attn(ctypes.byref(p.c()), ctypes.byref(cache), FAKE, FAKE, 2, FAKE, FAKE, FAKE,
+                            7, FAKE, 1 << 30, None)
+    assert st == snap.SNAP_ERR_INVALID_ARG
+    st = L.snap_cache_append(ctypes.byref(p.c()), ctypes.byref(cache), FAKE, 2, FAKE, FAKE, None, None)
+    assert st == snap.SNAP_ERR_INVALID_ARG  # v_new missing
+    assert L.snap_advance(FAKE, 0, 1, FAKE, None) == snap.SNAP_ERR_INVALID_ARG
+    assert L.snap_advance(FAKE, 4, 0, FAKE, None) == snap.SNAP_OK

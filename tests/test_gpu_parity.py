@@ -1,0 +1,166 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Every case prints what names it before touching the GPU.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2511_03092_amd as snap
+import synth
+from snaphelp import (TOL, GpuCache, check_compress, decode_steps, gpu_compress, oracle_params, params_of)
+
+pytestmark = pytest.mark.gpu
+
+BAND_RTOL = 5e-7  # pooled-score error near the threshold (implies the 1e-6 swap rule)
+ALL_RTOL = 1e-5   # pooled-score error anywhere (large planted logits carry more rounding)
+
+
+def _announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def _run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
+              check_every=1, fp8_scales=False):
+    q, k, v = synth.prefill_batch(wl, layer, lengths, salt=salt, pad_value=pad_value)
+    cache = GpuCache(p, n_slots)
+    if fp8_scales:
+        # per-(slot, head) scale = amax of the prompt rows / 448
+        for b, s_ in enumerate(slots):
+            L = lengths[b]
+            cache.k_scale[s_] = k[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6).cuda() / 448.0
+            if v is not None:
+                cache.v_scale[s_] = v[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6).cuda() / 448.0
+    sel, pooled = gpu_compress(p, cache, q, k, v, lengths, slots)
+    stats = check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
+    print(f"  swaps within tolerance: {stats['swaps']}, pooled max rel err: {stats['pooled_rel_err']:.3e}, "
+          f"decision band: {stats['band_rel_err']:.3e}", flush=True)
+    assert stats["band_rel_err"] <= BAND_RTOL and stats["pooled_rel_err"] <= ALL_RTOL
+    err = 0.0
+    if steps:
+        err = decode_steps(p, wl, cache, slots, steps, out_dtype, tol, check_every=check_every, layer=layer,
+                           salt=salt)
+        print(f"  decode max abs err over {steps} steps: {err:.3e}", flush=True)
+    return stats, err
+
+
+def test_tiny_fp32_workload():
+    wl = synth.WORKLOADS["tiny-fp32"]
+    _announce("tiny-fp32: L=1024, 4/2 heads, D64, budget 128, 16 decode steps")
+    p = params_of(wl)
+    _run_case(wl, p, [wl.length], [0], 1, wl.decode_steps, torch.float32, TOL["f32"])
+
+
+def test_llama_one_layer_32k_workload():
+    wl = synth.WORKLOADS["llama8b-1layer-32k"]
+    _announce("llama8b-1layer-32k: L=32768, 32/8 heads, budget 4096, 256 decode steps")
+    p = params_of(wl)
+    _run_case(wl, p, [wl.length], [0], 1, wl.decode_steps, torch.bfloat16, TOL["bf16"],
+                         check_every=8)
+
+
+MED = synth.Workload("med", 11, 8, 2, 128, 128, False, 4, 16, 300, 32, 13, "bf16", "bf16", layers=1, batch=3,
+                     length=None, length_range=(700, 5100), decode_steps=40, rope=True, plant_frac=0.01)
+
+
+@pytest.mark.parametrize("norm", [snap.SNAP_NORM_CAND, snap.SNAP_NORM_ROW])
+@pytest.mark.parametrize("pool", [snap.SNAP_POOL_MAX, snap.SNAP_POOL_AVG])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_variants_ragged_batch(norm, pool, dtype):
+    """Both normaliser domains and pool types, three ragged prompts padded with
+    NaN to one max_len, window (32) longer than the ring (16) so the causal
+    mask inside the window matters."""
+    wl = synth.small(MED, in_dtype=dtype, kv_dtype=dtype, pool=pool, norm=norm)
+    _announce(f"variants norm={norm} pool={pool} dtype={dtype}")
+    p = params_of(wl)
+    lengths = [5000, 777, 3001]
+    _run_case(wl, p, lengths, [2, 0, 1], 3, 24, torch.float32 if dtype == "f32" else torch.bfloat16,
+                         TOL[dtype])
+
+
+EDGE = synth.Workload("edge", 12, 4, 2, 64, 64, False, 4, 8, 16, 16, 5, "f32", "f32", layers=1, batch=1,
+                      length=None, length_range=(1, 100), decode_steps=12, rope=False, plant_count=3)
+
+
+@pytest.mark.parametrize("topk", [0, 16])
+def test_edge_lengths(topk):
+    """L = 0, 1, inside the sinks, inside sinks+ring (no candidates), exactly
+    sinks+ring, one candidate, candidates == K, one more than K, longer than
+    the window; decode steps then wrap the ring from every start."""
+    wl = synth.small(EDGE, topk=topk)
+    p = params_of(wl)
+    s, r = wl.sink, wl.recent
+    lengths = [0, 1, 3, s + 5, s + r, s + r + 1, s + r + topk, s + r + topk + 1, 90]
+    _announce(f"edge lengths {lengths} topk={topk}")
+    _run_case(wl, p, lengths, list(range(len(lengths))), len(lengths), 20, torch.float32, TOL["f32"])
+
+
+def test_invalid_slots_are_skipped():
+    wl = synth.small(EDGE, topk=16)
+    p = params_of(wl)
+    _announce("invalid slot ids -1 and n_slots are skipped")
+    lengths = [60, 70, 80]
+    q, k, v = synth.prefill_batch(wl, 0, lengths)
+    cache = GpuCache(p, 2)
+    cache.k.fill_(7.0)
+    cache.v.fill_(7.0)
+    slots = [-1, 1, 2]
+    sel, pooled = gpu_compress(p, cache, q, k, v, lengths, slots)
+    assert torch.all(cache.k[0] == 7.0) and torch.all(cache.v[0] == 7.0)
+    assert int(cache.pos[0]) == -1 and int(cache.pos[1]) == 70
+    check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
+    # decode on a batch that names a bad slot leaves everything else right
+    sl = torch.tensor([1, 5], dtype=torch.int32, device="cuda")
+    ws = snap.workspace(snap.snap_decode_workspace(p, 2))
+    out = torch.full((2, p.n_q_heads, p.d_v), 3.0, device="cuda")
+    qd, kn, vn = synth.decode_inputs(wl, 0, 0, [70, 0])
+    snap.snap_cache_append(p, cache.c(), cache.pos, sl, kn.cuda(), vn.cuda())
+    snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, qd.cuda(), out, ws)
+    snap.snap_advance(cache.pos, sl)
+    torch.cuda.synchronize()
+    assert torch.all(out[1] == 3.0)
+    assert int(cache.pos[1]) == 71
+    ck, cv = cache.host_values()
+    exp = oracle.decode_attn(oracle_params(p), [70], cache.n_topk.cpu().numpy()[[1]],
+                             qd[:1], ck[[1]], cv[[1]])
+    assert np.max(np.abs(out[:1].double().cpu().numpy() - exp)) <= TOL["f32"]
+
+
+def test_fp8_cache_continuous_batching_shape():
+    """fp8 E4M3 cache with per-(slot, head) scales, the continuous-batching
+    workload's budget split (768 sinks, 1024 recent, 6400 selected)."""
+    wl = synth.WORKLOADS["cb-fp8-llama8b-32slot"]
+    p = params_of(wl)
+    lengths = [9000, 20000]
+    _announce(f"fp8 cache lengths {lengths} into slots [5, 2] of 8")
+    _run_case(wl, p, lengths, [5, 2], 8, 32, torch.bfloat16, TOL["fp8"], fp8_scales=True,
+                         check_every=4)
+
+
+def test_mla_latent_cache_reduced_length():
+    """Latent (MLA) cache: 8 heads share one 576-wide row, values are its first
+    512 dims; the workload's split at a shorter prompt."""
+    wl = synth.small(synth.WORKLOADS["mla-8head-61layer-b16-128k"], recent=512, topk=2048)
+    p = params_of(wl)
+    lengths = [8192, 5000]
+    _announce(f"mla latent lengths {lengths}")
+    _run_case(wl, p, lengths, [1, 0], 2, 8, torch.bfloat16, TOL["bf16"])
+
+
+def test_compress_is_deterministic():
+    wl = synth.small(MED, norm=snap.SNAP_NORM_CAND)
+    p = params_of(wl)
+    lengths = [5000, 4096]
+    _announce("determinism: two identical compress calls")
+    q, k, v = synth.prefill_batch(wl, 0, lengths)
+    outs = []
+    for _ in range(2):
+        cache = GpuCache(p, 2)
+        sel, pooled = gpu_compress(p, cache, q, k, v, lengths, [0, 1])
+        outs.append((sel, pooled, cache.k.cpu(), cache.v.cpu()))
+    assert np.array_equal(outs[0][0], outs[1][0])
+    assert np.array_equal(outs[0][1], outs[1][1], equal_nan=True)
+    assert torch.equal(outs[0][2], outs[1][2]) and torch.equal(outs[0][3], outs[1][3])
