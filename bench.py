@@ -145,7 +145,7 @@ def main():
         valid += min(L + 1, s_r) + min(ncand, wl.topk)
     q_bytes = n * wl.n_q_heads * wl.d_qk * 2
     o_bytes = n * wl.n_q_heads * wl.d_v * 2
-    dec_bytes = valid * row_bytes + q_bytes + o_bytes
+    dec_bytes = valid * wl.n_kv_heads * row_bytes + q_bytes + o_bytes
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
     tokens = n * dsteps
     value = tokens / (ms_step * 1e-3)

@@ -159,10 +159,11 @@ __global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
-            float sacc = 0.f;
+            // fp32 products are exact in fp64; only the final rounding remains
+            double sacc = 0.0;
 #pragma unroll 4
-            for (int d = 0; d < D; ++d) sacc = fmaf(qrow[d], krow[d], sacc);
-            acc[rb][e] = sacc;
+            for (int d = 0; d < D; ++d) sacc = fma((double)qrow[d], (double)krow[d], sacc);
+            acc[rb][e] = (float)sacc;
           }
       }
       const int j = t0 + sb * 16 + l16;
@@ -251,7 +252,6 @@ struct ReduceArgs {
   float2* rowref;
   const int32_t* lengths;
   uint32_t* hist;      // [3][groups][kRadixBins]
-  uint32_t* done;      // [3][groups]
   RadixState* state;   // [groups]
   int groups, Hkv, max_len, sink, recent, topk;
   int rows_pad, n_kchunks;
@@ -260,34 +260,47 @@ struct ReduceArgs {
 // Row max m over every chunk and the normaliser.  The reference c is 0 when the
 // max lies in [-20, 64] (then exp(z) is taken directly, keeping the full fp32
 // accuracy of small logits), otherwise c = m; inv = 1 / sum_j exp(z_j - c),
-// accumulated in fp64.  Also resets this group's selection scratch.
+// accumulated in fp64.  Eight lanes share a row (chunks strided by 8) and
+// combine with in-wave shuffles; block 0 of each group also resets the
+// group's selection scratch.
+constexpr int kReduceLanes = 8;
 __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
-  const int bg = blockIdx.x, b = bg / a.Hkv;
+  const int bg = blockIdx.y, b = bg / a.Hkv;
+  const int sub = threadIdx.x % kReduceLanes;
+  const int rho = blockIdx.x * (256 / kReduceLanes) + threadIdx.x / kReduceLanes;
   const float2* st = a.stats + (size_t)bg * a.n_kchunks * a.rows_pad;
-  for (int rho = threadIdx.x; rho < a.rows_pad; rho += blockDim.x) {
+  if (rho < a.rows_pad) {
     float m = -INFINITY;
-    for (int c = 0; c < a.n_kchunks; ++c) m = fmaxf(m, st[(size_t)c * a.rows_pad + rho].x);
-    float2 ref = make_float2(0.f, 0.f);
+    for (int c = sub; c < a.n_kchunks; c += kReduceLanes) m = fmaxf(m, st[(size_t)c * a.rows_pad + rho].x);
+#pragma unroll
+    for (int o = 1; o < kReduceLanes; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+    double z = 0.0;
     if (m != -INFINITY) {
-      double z = 0.0;
-      for (int c = 0; c < a.n_kchunks; ++c) {
+      for (int c = sub; c < a.n_kchunks; c += kReduceLanes) {
         float2 v = st[(size_t)c * a.rows_pad + rho];
         if (v.x != -INFINITY) z += (double)v.y * exp((double)v.x - (double)m);
       }
-      if (m >= -20.f && m <= 64.f) {
-        ref.x = 0.f;
-        ref.y = (float)(1.0 / (z * exp((double)m)));
-      } else {
-        ref.x = m;
-        ref.y = (float)(1.0 / z);
-      }
     }
-    a.rowref[(size_t)bg * a.rows_pad + rho] = ref;
+#pragma unroll
+    for (int o = 1; o < kReduceLanes; o <<= 1) z += __shfl_xor(z, o);
+    if (sub == 0) {
+      float2 ref = make_float2(0.f, 0.f);
+      if (m != -INFINITY) {
+        if (m >= -20.f && m <= 64.f) {
+          ref.x = 0.f;
+          ref.y = (float)(1.0 / (z * exp((double)m)));
+        } else {
+          ref.x = m;
+          ref.y = (float)(1.0 / z);
+        }
+      }
+      a.rowref[(size_t)bg * a.rows_pad + rho] = ref;
+    }
   }
+  if (blockIdx.x != 0) return;
   for (int pass = 0; pass < 3; ++pass) {
     uint32_t* h = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
     for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) h[i] = 0u;
-    if (threadIdx.x == 0) a.done[pass * a.groups + bg] = 0u;
   }
   if (threadIdx.x == 0) {
     int L = a.lengths[b];
@@ -313,7 +326,6 @@ struct SelectArgs {
   float* pooled_out;     // optional [groups][max_len]
   const int32_t* lengths;
   uint32_t* hist;        // [3][groups][kRadixBins]
-  uint32_t* done;        // [3][groups]
   RadixState* state;     // [groups]
   uint2* counts;         // [groups][n_splits] (greater, equal)
   int32_t* sel;          // [groups][topk]
@@ -336,68 +348,34 @@ __device__ __forceinline__ uint32_t radix_digit(uint32_t bits, int pass) {
 __device__ __forceinline__ uint32_t radix_shift(int pass) { return pass == 0 ? 21u : (pass == 1 ? 10u : 0u); }
 __device__ __forceinline__ uint32_t radix_dmask(int pass) { return pass == 2 ? 0x3ffu : 0x7ffu; }
 
-// Publish the workgroup's LDS histogram; the last workgroup of the group then
-// finds the bin that holds the krem-th largest element (scanning from the top)
-// and narrows the threshold prefix.
-__device__ void radix_finish(const SelectArgs& a, int bg, int pass, uint32_t* lhist, uint32_t* lscratch) {
+// Each wave of a workgroup counts into its own LDS histogram (pooled scores of
+// neighbouring candidates share high bits, so one shared histogram would
+// serialise on a few bins); the four are summed and published with one
+// global atomic per non-empty bin.
+constexpr int kSubHists = kSelThreads / 64;
+__device__ __forceinline__ void radix_flush(const SelectArgs& a, int bg, int pass, uint32_t (*lhist)[kRadixBins]) {
   const int nb = pass == 2 ? 1024 : 2048;
   uint32_t* gh = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
   __syncthreads();
   for (int i = threadIdx.x; i < nb; i += blockDim.x) {
-    uint32_t v = lhist[i];
+    uint32_t v = 0;
+#pragma unroll
+    for (int w = 0; w < kSubHists; ++w) v += lhist[w][i];
     if (v) atomicAdd(&gh[i], v);
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t old = atomicAdd(&a.done[pass * a.groups + bg], 1u);
-    lscratch[0] = (old == (uint32_t)a.n_splits - 1u) ? 1u : 0u;
-  }
-  __syncthreads();
-  if (lscratch[0] == 0u) return;
-  __threadfence();
-  // last workgroup: wave 0 scans the global histogram
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const int per = nb / 64;  // 32 or 16 bins per lane
-    RadixState st = a.state[bg];
-    uint32_t hv[32];
-    uint32_t tot = 0;
-    for (int i = 0; i < per; ++i) {
-      hv[i] = __hip_atomic_load(&gh[lane * per + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      tot += hv[i];
-    }
-    // exclusive sum of the totals of higher lanes
-    uint32_t above = 0;
-    for (int o = 1; o < 64; ++o) {
-      uint32_t t = __shfl(tot, (lane + o) & 63);
-      if (lane + o < 64) above += t;
-    }
-    bool hit = above < (uint32_t)st.krem && above + tot >= (uint32_t)st.krem;
-    if (hit) {
-      uint32_t cum = above;
-      for (int i = per - 1; i >= 0; --i) {
-        if (cum + hv[i] >= (uint32_t)st.krem) {
-          uint32_t bin = (uint32_t)(lane * per + i);
-          st.krem -= (int32_t)cum;
-          st.prefix |= bin << radix_shift(pass);
-          st.mask |= radix_dmask(pass) << radix_shift(pass);
-          a.state[bg] = st;
-          break;
-        }
-        cum += hv[i];
-      }
-    }
-  }
+}
+
+__device__ __forceinline__ void clear_hists(uint32_t (*lhist)[kRadixBins]) {
+  for (int i = threadIdx.x; i < kSubHists * kRadixBins; i += blockDim.x) (&lhist[0][0])[i] = 0u;
 }
 
 // P = pool(A) on this workgroup's candidates (+ the debug copy) and the first
 // radix digit.
 __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
   __shared__ float la[kCandChunk + 64];
-  __shared__ uint32_t lhist[kRadixBins];
-  __shared__ uint32_t lscratch[4];
+  __shared__ uint32_t lhist[kSubHists][kRadixBins];
   const int bg = blockIdx.y, split = blockIdx.x;
+  const int wave = threadIdx.x >> 6;
   int c0, c1;
   seq_range(a, bg, c0, c1);
   const int half = a.pool_kernel / 2;
@@ -410,7 +388,7 @@ __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
     for (int j = threadIdx.x; j < a.max_len; j += blockDim.x)
       if (j < c0 || j >= c1) po[j] = __builtin_nanf("");
   }
-  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) lhist[i] = 0u;
+  if (st.mode == 2) clear_hists(lhist);
   if (j0 < j1) {
     const float* Ag = a.A + (size_t)bg * a.max_len;
     const float padv = a.pool == SNAP_POOL_MAX ? -INFINITY : 0.f;
@@ -432,33 +410,72 @@ __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
       }
       Pg[j] = v;
       if (a.pooled_out) a.pooled_out[(size_t)bg * a.max_len + j] = v;
-      if (st.mode == 2) atomicAdd(&lhist[radix_digit(__float_as_uint(v), 0)], 1u);
+      if (st.mode == 2) atomicAdd(&lhist[wave][radix_digit(__float_as_uint(v), 0)], 1u);
     }
   }
-  if (st.mode == 2) radix_finish(a, bg, 0, lhist, lscratch);
+  if (st.mode == 2) radix_flush(a, bg, 0, lhist);
 }
 
 __global__ __launch_bounds__(kSelThreads) void radix_pass(SelectArgs a, int pass) {
-  __shared__ uint32_t lhist[kRadixBins];
-  __shared__ uint32_t lscratch[4];
+  __shared__ uint32_t lhist[kSubHists][kRadixBins];
   const int bg = blockIdx.y, split = blockIdx.x;
+  const int wave = threadIdx.x >> 6;
   const RadixState st = a.state[bg];
   if (st.mode != 2) return;
   int c0, c1;
   seq_range(a, bg, c0, c1);
   const int j0 = c0 + split * kCandChunk, j1 = min(j0 + kCandChunk, c1);
-  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) lhist[i] = 0u;
+  clear_hists(lhist);
   __syncthreads();
   const float* Pg = a.P + (size_t)bg * a.max_len;
   for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
     uint32_t bits = __float_as_uint(Pg[j]);
-    if ((bits & st.mask) == st.prefix) atomicAdd(&lhist[radix_digit(bits, pass)], 1u);
+    if ((bits & st.mask) == st.prefix) atomicAdd(&lhist[wave][radix_digit(bits, pass)], 1u);
   }
-  radix_finish(a, bg, pass, lhist, lscratch);
+  radix_flush(a, bg, pass, lhist);
+}
+
+// One workgroup per group: find the bin that holds the krem-th largest of the
+// elements still matching the prefix, counting from the top bin down, and
+// narrow the threshold.  Thread t owns the 8 (or 4) bins just below the bins
+// of thread t-1, so its exclusive prefix is the count above its bins.
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total);
+__global__ __launch_bounds__(kSelThreads) void radix_scan(SelectArgs a, int pass) {
+  __shared__ uint32_t lds[8];
+  const int bg = blockIdx.x;
+  RadixState st = a.state[bg];
+  if (st.mode != 2) return;
+  const int nb = pass == 2 ? 1024 : 2048;
+  const int per = nb / kSelThreads;  // 8 or 4
+  const uint32_t* gh = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
+  const int top = nb - per * threadIdx.x;  // this thread's bins: [top - per, top)
+  uint32_t hv[8];
+  uint32_t tot = 0;
+  for (int i = 0; i < per; ++i) {
+    hv[i] = gh[top - 1 - i];
+    tot += hv[i];
+  }
+  uint32_t total;
+  const uint32_t above = block_exclusive_scan(tot, lds, total);
+  const uint32_t krem = (uint32_t)st.krem;
+  if (above < krem && above + tot >= krem) {
+    uint32_t cum = above;
+    for (int i = 0; i < per; ++i) {
+      if (cum + hv[i] >= krem) {
+        uint32_t bin = (uint32_t)(top - 1 - i);
+        st.krem -= (int32_t)cum;
+        st.prefix |= bin << radix_shift(pass);
+        st.mask |= radix_dmask(pass) << radix_shift(pass);
+        a.state[bg] = st;
+        break;
+      }
+      cum += hv[i];
+    }
+  }
 }
 
 // block-wide exclusive scan of one value per thread (kSelThreads threads)
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total) {
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t x = v;
 #pragma unroll
@@ -705,8 +722,6 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   off = align256(off + (size_t)groups * max_len * sizeof(float));
   g.off_hist = off;
   off = align256(off + (size_t)3 * groups * kRadixBins * sizeof(uint32_t));
-  g.off_done = off;
-  off = align256(off + (size_t)3 * groups * sizeof(uint32_t));
   g.off_state = off;
   off = align256(off + (size_t)groups * sizeof(RadixState));
   g.off_counts = off;
@@ -764,7 +779,6 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   float* A = (float*)(w + geo.off_A);
   float* P = (float*)(w + geo.off_P);
   uint32_t* hist = (uint32_t*)(w + geo.off_hist);
-  uint32_t* done = (uint32_t*)(w + geo.off_done);
   RadixState* state = (RadixState*)(w + geo.off_state);
   uint2* counts = (uint2*)(w + geo.off_counts);
   int32_t* sel = (int32_t*)(w + geo.off_sel);
@@ -802,7 +816,6 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   ra.rowref = rowref;
   ra.lengths = lengths;
   ra.hist = hist;
-  ra.done = done;
   ra.state = state;
   ra.groups = groups;
   ra.Hkv = p.n_kv_heads;
@@ -812,7 +825,7 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   ra.topk = p.topk;
   ra.rows_pad = geo.rows_pad;
   ra.n_kchunks = geo.n_kchunks;
-  hipLaunchKernelGGL(stats_reduce, dim3(groups), dim3(256), 0, stream, ra);
+  hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + 31) / 32, groups), dim3(256), 0, stream, ra);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
 
   e = bf ? launch_score<uint16_t>(sa, p.d_qk, nwaves, true, groups, geo.n_kchunks, stream)
@@ -825,7 +838,6 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   se.pooled_out = pooled_out;
   se.lengths = lengths;
   se.hist = hist;
-  se.done = done;
   se.state = state;
   se.counts = counts;
   se.sel = sel;
@@ -840,8 +852,11 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   se.n_splits = geo.n_splits;
   dim3 sgrid(geo.n_splits, groups);
   hipLaunchKernelGGL(pool_hist0, sgrid, dim3(kSelThreads), 0, stream, se);
+  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 0);
   hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 1);
+  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 1);
   hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 2);
+  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 2);
   hipLaunchKernelGGL(select_count, sgrid, dim3(kSelThreads), 0, stream, se);
   hipLaunchKernelGGL(select_write, sgrid, dim3(kSelThreads), 0, stream, se);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;

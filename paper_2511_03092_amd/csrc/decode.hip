@@ -73,13 +73,34 @@ __device__ __forceinline__ u32x4 e4m3x8_to_bf16x8(u32x2 c) {
   return o;
 }
 
+// Raw 8-element loads: bf16 rows stay as 16 bytes, fp8 rows as 8 bytes of codes
+// until they are used, so a prefetch does not wait on a conversion.
 template <bool FP8>
-__device__ __forceinline__ u32x4 load8(const void* base, size_t elem) {
-  if constexpr (FP8) {
-    return e4m3x8_to_bf16x8(*(const u32x2*)((const uint8_t*)base + elem));
-  } else {
+struct Raw8 {
+  typedef u32x4 T;
+};
+template <>
+struct Raw8<true> {
+  typedef u32x2 T;
+};
+
+template <bool FP8>
+__device__ __forceinline__ typename Raw8<FP8>::T load_raw8(const void* base, size_t elem, bool ok) {
+  typedef typename Raw8<FP8>::T T;
+  T z = {};
+  if (!ok) return z;
+  if constexpr (FP8)
+    return *(const u32x2*)((const uint8_t*)base + elem);
+  else
     return *(const u32x4*)((const uint16_t*)base + elem);
-  }
+}
+
+template <bool FP8>
+__device__ __forceinline__ u32x4 bf16x8_of(typename Raw8<FP8>::T r) {
+  if constexpr (FP8)
+    return e4m3x8_to_bf16x8(r);
+  else
+    return r;
 }
 
 // ---------------------------------------------------------------- MFMA decode
@@ -89,6 +110,7 @@ __device__ __forceinline__ u32x4 load8(const void* base, size_t elem) {
 template <int KSTEPS, int VPASS, bool FP8>
 __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   constexpr int D = KSTEPS * 32;
+  typedef typename Raw8<FP8>::T RawT;
   const int lane = threadIdx.x, l16 = lane & 15, lg = lane >> 4;
   const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
   int slot;
@@ -124,36 +146,39 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[pp][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int vb = sp.v0; vb < sp.v1; vb += 32) {
-    // ---- loads: two 16-row K sets, eight V rows per lane
-    u32x4 ka[KSTEPS], kb[KSTEPS];
-    {
-      const int va = vb + l16, vb2 = vb + 16 + l16;
-      const bool oka = va < sp.v1, okb = vb2 < sp.v1;
-      const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
+  // K of block vb: lane's rows vb+l16 and vb+16+l16, k-slot group lg
+  auto load_k = [&](int vb, RawT* ka, RawT* kb) {
+    const int va = vb + l16, vb2 = vb + 16 + l16;
+    const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
 #pragma unroll
-      for (int t = 0; t < KSTEPS; ++t) {
-        const int col = 8 * (KSTEPS * lg + t);
-        ka[t] = oka ? load8<FP8>(a.ck, ra * D + col) : u32x4{0u, 0u, 0u, 0u};
-        kb[t] = okb ? load8<FP8>(a.ck, rb * D + col) : u32x4{0u, 0u, 0u, 0u};
-      }
+    for (int t = 0; t < KSTEPS; ++t) {
+      const int col = 8 * (KSTEPS * lg + t);
+      ka[t] = load_raw8<FP8>(a.ck, ra * D + col, va < sp.v1);
+      kb[t] = load_raw8<FP8>(a.ck, rb * D + col, vb2 < sp.v1);
     }
-    u32x4 vv[VPASS][8];
+  };
+  RawT ka[KSTEPS], kb[KSTEPS];
+  if (sp.v0 < sp.v1) load_k(sp.v0, ka, kb);
+
+  for (int vb = sp.v0; vb < sp.v1; vb += 32) {
+    // V of this block (eight rows per lane, in the order of the score layout),
+    // then K of the next block: the value product waits only for V.
+    RawT vv[VPASS][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
-      const bool ok = vi < sp.v1;
       const size_t rr = row0 + virt_row(vi, sp.n1, sr);
 #pragma unroll
-      for (int pp = 0; pp < VPASS; ++pp)
-        vv[pp][i] = ok ? load8<FP8>(vbase, rr * vstride + 128 * pp + 8 * l16) : u32x4{0u, 0u, 0u, 0u};
+      for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(vbase, rr * vstride + 128 * pp + 8 * l16, vi < sp.v1);
     }
-    // ---- S^T = K q^T for 32 rows
+    RawT kn[KSTEPS], kn2[KSTEPS];
+    if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
+
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < KSTEPS; ++t) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[t]), qf[t], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kb[t]), qf[t], s1, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(ka[t])), qf[t], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(kb[t])), qf[t], s1, 0, 0, 0);
     }
     float x[8];
 #pragma unroll
@@ -180,19 +205,27 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-    // ---- O^T += V^T P^T
 #pragma unroll
-    for (int pp = 0; pp < VPASS; ++pp)
+    for (int pp = 0; pp < VPASS; ++pp) {
+      u32x4 vbf[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) vbf[i] = bf16x8_of<FP8>(vv[pp][i]);
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const int u = c >> 1;
         const uint32_t selb = (c & 1) ? 0x07060302u : 0x05040100u;
         u32x4 av;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vv[pp][2 * i + 1][u], vv[pp][2 * i][u], selb);
+        for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vbf[2 * i + 1][u], vbf[2 * i][u], selb);
         acc[pp][c] *= alpha;
         acc[pp][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[pp][c], 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      ka[t] = kn[t];
+      kb[t] = kn2[t];
+    }
   }
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
@@ -228,6 +261,7 @@ __device__ __forceinline__ int mla_kcnt(int w) { return w < 2 ? 5 : 4; }
 template <bool FP8>
 __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
   constexpr int D = kMlaKSteps * 32;  // 576
+  typedef typename Raw8<FP8>::T RawT;
   __shared__ f32x4 sbuf[2][4][2][64];  // [parity][wave][row set][lane]
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
@@ -260,34 +294,38 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  auto load_k = [&](int vb, RawT* ka, RawT* kbv) {
+    const int va = vb + l16, vb2 = vb + 16 + l16;
+    const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      const int col = 32 * kb + 8 * (kc * lg + t);
+      const bool tin = t < kc;
+      ka[t] = load_raw8<FP8>(a.ck, ra * D + col, va < sp.v1 && tin);
+      kbv[t] = load_raw8<FP8>(a.ck, rb * D + col, vb2 < sp.v1 && tin);
+    }
+  };
+  RawT ka[5], kbv[5];
+  if (sp.v0 < sp.v1) load_k(sp.v0, ka, kbv);
+
   int parity = 0;
   for (int vb = sp.v0; vb < sp.v1; vb += 32, parity ^= 1) {
-    u32x4 ka[5], kbv[5];
-    {
-      const int va = vb + l16, vb2 = vb + 16 + l16;
-      const bool oka = va < sp.v1, okb = vb2 < sp.v1;
-      const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
-#pragma unroll
-      for (int t = 0; t < 5; ++t) {
-        const int col = 32 * kb + 8 * (kc * lg + t);
-        const bool tin = t < kc;
-        ka[t] = (oka && tin) ? load8<FP8>(a.ck, ra * D + col) : u32x4{0u, 0u, 0u, 0u};
-        kbv[t] = (okb && tin) ? load8<FP8>(a.ck, rb * D + col) : u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-    u32x4 vv[8];
+    RawT vv[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
       const size_t rr = row0 + virt_row(vi, sp.n1, sr);
-      vv[i] = vi < sp.v1 ? load8<FP8>(a.ck, rr * D + 128 * w + 8 * l16) : u32x4{0u, 0u, 0u, 0u};
+      vv[i] = load_raw8<FP8>(a.ck, rr * D + 128 * w + 8 * l16, vi < sp.v1);
     }
+    RawT kn[5], kn2[5];
+    if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
+
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < 5; ++t) {
       if (t < kc) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[t]), qf[t], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kbv[t]), qf[t], s1, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(ka[t])), qf[t], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(kbv[t])), qf[t], s1, 0, 0, 0);
       }
     }
     sbuf[parity][w][0][lane] = s0;
@@ -320,15 +358,23 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+    u32x4 vbf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) vbf[i] = bf16x8_of<FP8>(vv[i]);
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int u = c >> 1;
       const uint32_t selb = (c & 1) ? 0x07060302u : 0x05040100u;
       u32x4 av;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vv[2 * i + 1][u], vv[2 * i][u], selb);
+      for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vbf[2 * i + 1][u], vbf[2 * i][u], selb);
       acc[c] *= alpha;
       acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[c], 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      ka[t] = kn[t];
+      kbv[t] = kn2[t];
     }
   }
   lsum += __shfl_xor(lsum, 16);
@@ -430,33 +476,58 @@ struct CombineArgs {
   int Hq, dv, n_chunks, n_slots, out_bf16;
 };
 
-__global__ __launch_bounds__(256) void combine(CombineArgs a) {
+constexpr int kMaxChunks = 512;
+constexpr int kCombineThreads = 128;
+// grid (n * Hq, ceil(dv / 128)): the chunk weights exp2(m_c - M) are formed
+// once per workgroup in LDS, then each thread sums its value dim over chunks.
+__global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
+  __shared__ float wts[kMaxChunks];
+  __shared__ float red[kCombineThreads / 64];
   const int bh = blockIdx.x, b = bh / a.Hq;
   const int slot = a.slot_ids[b];
   if (slot < 0 || slot >= a.n_slots) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float2* ml = a.ml + (size_t)bh * a.n_chunks;
   float M = -INFINITY;
-  for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, ml[c].x);
-  float wsum = 0.f;
-  for (int c = 0; c < a.n_chunks; ++c) {
+  for (int c = threadIdx.x; c < a.n_chunks; c += blockDim.x) M = fmaxf(M, ml[c].x);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if (lane == 0) red[wave] = M;
+  __syncthreads();
+  M = red[0];
+  for (int i = 1; i < kCombineThreads / 64; ++i) M = fmaxf(M, red[i]);
+  __syncthreads();
+  float ws = 0.f;
+  for (int c = threadIdx.x; c < a.n_chunks; c += blockDim.x) {
     float2 v = ml[c];
-    if (v.x != -INFINITY) wsum += exp2f(v.x - M) * v.y;
+    float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : exp2f(v.x - M);
+    wts[c] = wc;
+    ws += wc * v.y;
   }
+  ws = warp_sum(ws);
+  if (lane == 0) red[wave] = ws;
+  __syncthreads();
+  float wsum = 0.f;
+  for (int i = 0; i < kCombineThreads / 64; ++i) wsum += red[i];
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  const float* part = a.part + (size_t)bh * a.n_chunks * a.dv;
-  for (int d = threadIdx.x; d < a.dv; d += blockDim.x) {
-    float o = 0.f;
-    for (int c = 0; c < a.n_chunks; ++c) {
-      float mc = ml[c].x;
-      if (mc != -INFINITY) o = fmaf(exp2f(mc - M), part[(size_t)c * a.dv + d], o);
-    }
-    o *= inv;
-    size_t oi = (size_t)bh * a.dv + d;
-    if (a.out_bf16)
-      ((uint16_t*)a.out)[oi] = (uint16_t)f32_to_bf16_bits(o);
-    else
-      ((float*)a.out)[oi] = o;
+  const int d = blockIdx.y * kCombineThreads + threadIdx.x;
+  if (d >= a.dv) return;
+  const float* part = a.part + (size_t)bh * a.n_chunks * a.dv + d;
+  float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+  int c = 0;
+  for (; c + 4 <= a.n_chunks; c += 4) {
+    o0 = fmaf(wts[c], part[(size_t)c * a.dv], o0);
+    o1 = fmaf(wts[c + 1], part[(size_t)(c + 1) * a.dv], o1);
+    o2 = fmaf(wts[c + 2], part[(size_t)(c + 2) * a.dv], o2);
+    o3 = fmaf(wts[c + 3], part[(size_t)(c + 3) * a.dv], o3);
   }
+  for (; c < a.n_chunks; ++c) o0 = fmaf(wts[c], part[(size_t)c * a.dv], o0);
+  const float o = ((o0 + o1) + (o2 + o3)) * inv;
+  const size_t oi = (size_t)bh * a.dv + d;
+  if (a.out_bf16)
+    ((uint16_t*)a.out)[oi] = (uint16_t)f32_to_bf16_bits(o);
+  else
+    ((float*)a.out)[oi] = o;
 }
 
 // ---------------------------------------------------------------- append / advance
@@ -544,9 +615,14 @@ Geometry decode_geometry(const snap_params& p, int n) {
   Geometry g{};
   const int B = p.sink + p.recent + p.topk;
   const int units = (n > 0 ? n : 1) * p.n_kv_heads;
-  int want = (2048 + units - 1) / units;
-  int maxc = (B + 63) / 64;
+  // latent caches run 4-wave workgroups (two per CU), the others one wave each
+  const bool latent = p.v_in_k && p.d_qk == 576;
+  const int target = latent ? 512 : 2048;
+  const int min_rows = latent ? 256 : 128;
+  int want = (target + units - 1) / units;
+  int maxc = (B + min_rows - 1) / min_rows;
   if (maxc < 1) maxc = 1;
+  if (maxc > kMaxChunks) maxc = kMaxChunks;
   g.n_chunks = want < 1 ? 1 : (want > maxc ? maxc : want);
   size_t off = 0;
   g.off_part = off;
@@ -621,7 +697,8 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
   ca.n_chunks = geo.n_chunks;
   ca.n_slots = c.n_slots;
   ca.out_bf16 = out_dtype == SNAP_BF16;
-  hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads), dim3(128), 0, stream, ca);
+  hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads, (p.d_v + kCombineThreads - 1) / kCombineThreads),
+                     dim3(kCombineThreads), 0, stream, ca);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
   return SNAP_OK;
 }
