@@ -32,23 +32,221 @@ struct ScoreArgs {
   float* A;             // [n_seq*Hkv][max_len]
   int Hq, Hkv, G, w, max_len, sink, recent, norm;
   int rows, rows_pad, key_chunk, n_kchunks;
-  float scale;
+  float scale;   // softmax scale
+  float scale2;     // scale * log2(e) rounded to fp32: logits in log2 units
+  float scale2_lo;  // scale * log2(e) - scale2
 };
+
+// LDS tile of kKeyTile = 64 keys stored chunk-major: the 16-byte chunk c of key
+// k sits at slot c*64 + k.  A fragment read by 16 consecutive keys of one
+// chunk is 256 contiguous bytes (all 64 banks once), and in every tile load
+// lane = key, so a lane needs one row pointer and the chunk offset is uniform.
+__device__ __forceinline__ int tile_slot(int key, int c) { return c * kKeyTile + key; }
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// One wave-instruction of global -> LDS copy: lane i's 16 bytes at g land at
+// LDS byte lds_wave_base + 16*i.  Issued through inline asm so that the only
+// ordering with later LDS reads is the explicit vmcnt wait + barrier of the
+// caller (the compiler's own LDS-DMA tracking would otherwise wait for every
+// tile in flight).  M0 (the LDS base of the DMA) is saved and restored, with
+// the one wait state an M0 write needs before an LDS DMA.
+__device__ __forceinline__ void dma16(const void* g, const void* lds_wave_base) {
+  const uint32_t la = (uint32_t)(uintptr_t)(lds_void_ptr)lds_wave_base;
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(la), "v"(g)
+      : "memory");
+}
+
+// Issue this wave's share of one key tile: CPR wave-instructions per tile
+// (chunk c = wave + ii*NW), each moving 64 x 16 bytes straight into LDS (no
+// VGPRs).  Keys past c1 read key c1-1 instead so every wave always issues the
+// same number of loads (those bytes are never used).
+template <int CPR, int NW>
+__device__ __forceinline__ void issue_tile(const unsigned char* kbase, size_t row_bytes, int t0, int c1,
+                                           unsigned char* buf, int wave, int lane) {
+  static_assert(CPR % NW == 0, "tile loads must split evenly over the waves");
+  static_assert(kKeyTile == 64, "one key per lane");
+  int j = t0 + lane;
+  j = j < c1 ? j : c1 - 1;
+  const unsigned char* rowp = kbase + (size_t)j * row_bytes;
+  const int w = __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+  for (int ii = 0; ii < CPR / NW; ++ii) {
+    const int c = w + ii * NW;
+    dma16(rowp + c * 16, buf + (size_t)c * 1024);
+  }
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N < 64, "vmcnt field");
+  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier that waits only for this wave's LDS traffic (not for its
+// in-flight global->LDS tile loads, which are counted separately), and keeps
+// the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt, expcnt untouched
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+struct ScoreLane {
+  int rpos[2][4];
+  bool rval[2][4];
+  float rm[2][4], rz[2][4], rc[2][4], rinv[2][4], rinvl[2][4];  // rinvl = rinv * ln2
+};
+
+// Normalised weight of one logit: 2^(y - c) * inv with y = acc * (s2 + s2lo).
+// y is formed as the rounded product yh plus its exact error and the part of
+// scale*log2(e) that fp32 s2 dropped; that small remainder enters to first
+// order, 2^(yh + yl - c) = 2^(yh - c) * (1 + yl*ln2), folded into the row factor.
+__device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c, float inv, float invl) {
+  const float yh = acc * s2;
+  float yl = fmaf(acc, s2, -yh);
+  yl = fmaf(acc, s2lo, yl);
+  return exp2f(yh - c) * fmaf(yl, invl, inv);
+}
+
+// One 64-key tile already resident in LDS: scores for this wave's 32 rows,
+// then either the running row max / sum of powers of two (STATS) or the
+// column sums of the normalised weights written to A (COLSUM).  Logits are
+// kept in log2 units, y = <q,k> * scale * log2(e), formed by one rounded
+// multiply, so exp(z) = exp2(y).  `interior` (uniform) means every key of the
+// tile is a candidate that precedes every window row: no per-element masks.
+template <typename In, int KSTEPS, int NW, bool COLSUM>
+__device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned char* __restrict__ ktile,
+                                           const bf16x8 (&qf)[2][KSTEPS], const float* qlds, float* colbuf,
+                                           ScoreLane& sl, int t0, int c1, bool interior, int bg, int wave,
+                                           int lane, bool wave_has_rows) {
+  constexpr bool kBF16 = sizeof(In) == 2;
+  constexpr int D = KSTEPS * 32;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const float s2 = a.scale2, s2lo = a.scale2_lo;
+  float xv[2][4][kKeyTile / 16];
+#pragma unroll
+  for (int sb = 0; sb < kKeyTile / 16; ++sb) {
+    f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    const int key = sb * 16 + l16;
+    if (wave_has_rows) {
+      if constexpr (kBF16) {
+#pragma unroll
+        for (int t = 0; t < KSTEPS; ++t) {
+          bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot(key, KSTEPS * lg + t) * 16));
+          acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
+          acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
+            // fp32 products are exact in fp64; only the final rounding remains
+            double sacc = 0.0;
+#pragma unroll 4
+            for (int d = 0; d < D; ++d) {
+              const float kd = *(const float*)(ktile + (size_t)tile_slot(key, d >> 2) * 16 + (d & 3) * 4);
+              sacc = fma((double)qrow[d], (double)kd, sacc);
+            }
+            acc[rb][e] = (float)sacc;
+          }
+      }
+    }
+    const int j = t0 + key;
+    float colv[2][4];
+    if (interior) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (!COLSUM)
+            xv[rb][e][sb] = acc[rb][e] * s2;
+          else
+            colv[rb][e] = weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]);
+        }
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool in = sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e];
+          if (!COLSUM)
+            xv[rb][e][sb] = in ? acc[rb][e] * s2 : -INFINITY;
+          else
+            colv[rb][e] = in ? weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]) : 0.f;
+        }
+    }
+    if (COLSUM) {
+      float cs = ((colv[0][0] + colv[0][1]) + (colv[0][2] + colv[0][3])) +
+                 ((colv[1][0] + colv[1][1]) + (colv[1][2] + colv[1][3]));
+      cs += __shfl_xor(cs, 16);
+      cs += __shfl_xor(cs, 32);
+      if (lg == 0) colbuf[wave * kKeyTile + sb * 16 + l16] = cs;
+    }
+  }
+  if (!COLSUM) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float mt = fmaxf(fmaxf(xv[rb][e][0], xv[rb][e][1]), fmaxf(xv[rb][e][2], xv[rb][e][3]));
+        float mn = fmaxf(sl.rm[rb][e], mt);
+        if (mn == -INFINITY) continue;
+        float z = sl.rz[rb][e] * exp2f(sl.rm[rb][e] - mn);
+        z += (exp2f(xv[rb][e][0] - mn) + exp2f(xv[rb][e][1] - mn)) + (exp2f(xv[rb][e][2] - mn) + exp2f(xv[rb][e][3] - mn));
+        sl.rz[rb][e] = z;
+        sl.rm[rb][e] = mn;
+      }
+  } else {
+    lds_barrier();
+    if (threadIdx.x < kKeyTile) {
+      int j = t0 + threadIdx.x;
+      const float* c = colbuf + threadIdx.x;
+      float sum;
+      if constexpr (NW == 4) {
+        sum = (c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile]);
+      } else {
+        sum = ((c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile])) +
+              ((c[4 * kKeyTile] + c[5 * kKeyTile]) + (c[6 * kKeyTile] + c[7 * kKeyTile]));
+      }
+      if (j < c1) a.A[(size_t)bg * a.max_len + j] = sum;
+    }
+  }
+}
 
 // Row state of one lane: the MFMA 16x16 output gives lane l the rows
 // 4*(l/16)+e (e = 0..3) of each 16-row block and the key column l%16.
-template <typename In, int KSTEPS, bool COLSUM>
-__global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
+// NW waves per workgroup; wave w owns score rows [32w, 32w+32).  Key tiles
+// are double-buffered in two LDS arrays (the loop is unrolled by two so each
+// half reads one array while the loads of the next tile fill the other).
+template <typename In, int KSTEPS, int NW, bool COLSUM>
+__global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
   constexpr bool kBF16 = sizeof(In) == 2;
   constexpr int D = KSTEPS * 32;
-  constexpr int kPitch = D * (int)sizeof(In) + 16;  // padded LDS row (bytes)
-  extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* ktile = smem;                                   // [kKeyTile][kPitch]
-  float* colbuf = (float*)(smem + kKeyTile * kPitch);            // [waves][kKeyTile]
-  float* qlds = colbuf + 8 * kKeyTile;                           // fp32 inputs: [rows_pad][D]
+  constexpr int kRowBytes = D * (int)sizeof(In);
+  constexpr int CPR = kRowBytes / 16;                 // 16-byte chunks per key row
+  constexpr int kTileBytes = kKeyTile * kRowBytes;
+  constexpr int IPW = CPR / NW;                        // tile loads per wave
+  __shared__ __align__(16) unsigned char tile0[kTileBytes];
+  __shared__ __align__(16) unsigned char tile1[kTileBytes];
+  __shared__ float colbuf[NW * kKeyTile];
+  __shared__ float qlds[kBF16 ? 1 : 128 * D];           // fp32 inputs: [rows_pad <= 128][D]
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
   const int bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
   int L = a.lengths[b];
@@ -66,18 +264,17 @@ __global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
   const int c0 = lo + blockIdx.x * a.key_chunk;
   const int c1 = min(c0 + a.key_chunk, hi);
   const int we = min(a.w, L);
+  const bool wave_has_rows = wave * 32 < a.rows;
 
-  // positions and validity of this lane's 8 rows
-  int rpos[2][4];
-  bool rval[2][4];
+  ScoreLane sl;
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       int rho = wave * 32 + rb * 16 + lg * 4 + e;
       int ii = rho % a.w;
-      rval[rb][e] = rho < a.rows && ii >= a.w - we;
-      rpos[rb][e] = L - a.w + ii;
+      sl.rval[rb][e] = rho < a.rows && ii >= a.w - we;
+      sl.rpos[rb][e] = L - a.w + ii;
     }
 
   float2* st_out = a.stats + ((size_t)bg * a.n_kchunks + blockIdx.x) * a.rows_pad;
@@ -87,6 +284,9 @@ __global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
     }
     return;
   }
+
+  const unsigned char* kbase =
+      (const unsigned char*)a.k + ((size_t)b * a.Hkv + g) * (size_t)a.max_len * kRowBytes;
 
   // ---- query rows of this wave
   const In* qbase = (const In*)a.q + ((size_t)b * a.Hq + (size_t)g * a.G) * a.w * D;
@@ -111,117 +311,56 @@ __global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
     }
   }
 
-  float rm[2][4], rz[2][4], rc[2][4], rinv[2][4];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      rm[rb][e] = -INFINITY;
-      rz[rb][e] = 0.f;
+      sl.rm[rb][e] = -INFINITY;
+      sl.rz[rb][e] = 0.f;
       if (COLSUM) {
         int rho = wave * 32 + rb * 16 + lg * 4 + e;
-        float2 rf = a.rowref[(size_t)bg * a.rows_pad + rho];
-        rc[rb][e] = rf.x;
-        rinv[rb][e] = rval[rb][e] ? rf.y : 0.f;
+        float2 rf = rho < a.rows_pad ? a.rowref[(size_t)bg * a.rows_pad + rho] : make_float2(0.f, 0.f);
+        sl.rc[rb][e] = sl.rval[rb][e] ? rf.x : 0.f;  // already in log2 units
+        sl.rinv[rb][e] = sl.rval[rb][e] ? rf.y : 0.f;
+        sl.rinvl[rb][e] = sl.rinv[rb][e] * 0.69314718055994531f;
       }
     }
+  // The query fragments and row normalisers must have landed before the first
+  // tile load is issued: the loop's waits only count tile loads.
+  wait_vm<0>();
+  issue_tile<CPR, NW>(kbase, kRowBytes, c0, c1, tile0, wave, lane);
 
-  const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * a.Hkv + g) * (size_t)a.max_len * D * sizeof(In);
-  constexpr int kChunks16 = D * (int)sizeof(In) / 16;  // 16-byte pieces per key row
+  // a tile is interior when all its keys are in range and precede the first
+  // window position (rows of negative position exist only when L < w)
+  const int first_row_pos = L - a.w;
+  auto interior_of = [&](int t) { return t + kKeyTile <= c1 && t + kKeyTile - 1 <= first_row_pos; };
 
-  for (int t0 = c0; t0 < c1; t0 += kKeyTile) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < kKeyTile * kChunks16; i += blockDim.x) {
-      int kk = i / kChunks16, pc = i % kChunks16;
-      int j = t0 + kk;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (j < c1) v = *(const u32x4*)(kbase + (size_t)j * D * sizeof(In) + pc * 16);
-      *(u32x4*)(ktile + kk * kPitch + pc * 16) = v;
-    }
-    __syncthreads();
-
-    float xv[2][4][kKeyTile / 16];
-#pragma unroll
-    for (int sb = 0; sb < kKeyTile / 16; ++sb) {
-      f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-      if constexpr (kBF16) {
-        const unsigned char* krow = ktile + (sb * 16 + l16) * kPitch;
-#pragma unroll
-        for (int t = 0; t < KSTEPS; ++t) {
-          bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(krow + 16 * (KSTEPS * lg + t)));
-          acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
-          acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
-        }
+  // two tiles per iteration: tile0 <- even tiles, tile1 <- odd tiles
+  for (int t0 = c0; t0 < c1; t0 += 2 * kKeyTile) {
+    {
+      lds_barrier();  // every wave is done reading tile1
+      if (t0 + kKeyTile < c1) {
+        issue_tile<CPR, NW>(kbase, kRowBytes, t0 + kKeyTile, c1, tile1, wave, lane);
+        wait_vm<IPW>();
       } else {
-        const float* krow = (const float*)(ktile + (sb * 16 + l16) * kPitch);
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
-            // fp32 products are exact in fp64; only the final rounding remains
-            double sacc = 0.0;
-#pragma unroll 4
-            for (int d = 0; d < D; ++d) sacc = fma((double)qrow[d], (double)krow[d], sacc);
-            acc[rb][e] = (float)sacc;
-          }
+        wait_vm<0>();
       }
-      const int j = t0 + sb * 16 + l16;
-      float colv[2][4];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bool in = rval[rb][e] && j < c1 && j <= rpos[rb][e];
-          float x = acc[rb][e] * a.scale;
-          if (!COLSUM) {
-            xv[rb][e][sb] = in ? x : -INFINITY;
-          } else {
-            colv[rb][e] = in ? expf(x - rc[rb][e]) * rinv[rb][e] : 0.f;
-          }
-        }
-      if (COLSUM) {
-        float cs = ((colv[0][0] + colv[0][1]) + (colv[0][2] + colv[0][3])) +
-                   ((colv[1][0] + colv[1][1]) + (colv[1][2] + colv[1][3]));
-        cs += __shfl_xor(cs, 16);
-        cs += __shfl_xor(cs, 32);
-        if (lg == 0) colbuf[wave * kKeyTile + sb * 16 + l16] = cs;
-      }
+      lds_barrier();  // tile0 holds keys [t0, t0+64)
+      score_tile<In, KSTEPS, NW, COLSUM>(a, tile0, qf, qlds, colbuf, sl, t0, c1, interior_of(t0), bg, wave, lane,
+                                         wave_has_rows);
     }
-
-    if (!COLSUM) {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float mt = xv[rb][e][0];
-#pragma unroll
-          for (int sb = 1; sb < kKeyTile / 16; ++sb) mt = fmaxf(mt, xv[rb][e][sb]);
-          float mn = fmaxf(rm[rb][e], mt);
-          if (mn == -INFINITY) continue;
-          float z = rz[rb][e] * __expf(rm[rb][e] - mn);
-#pragma unroll
-          for (int sb = 0; sb < kKeyTile / 16; ++sb) z += __expf(xv[rb][e][sb] - mn);
-          rz[rb][e] = z;
-          rm[rb][e] = mn;
-        }
-    } else {
-      __syncthreads();
-      if (threadIdx.x < kKeyTile) {
-        int j = t0 + threadIdx.x;
-        float sum = 0.f;
-        if (nwaves == 4) {
-          sum = (colbuf[threadIdx.x] + colbuf[kKeyTile + threadIdx.x]) +
-                (colbuf[2 * kKeyTile + threadIdx.x] + colbuf[3 * kKeyTile + threadIdx.x]);
-        } else if (nwaves == 8) {
-          const float* c = colbuf + threadIdx.x;
-          sum = ((c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile])) +
-                ((c[4 * kKeyTile] + c[5 * kKeyTile]) + (c[6 * kKeyTile] + c[7 * kKeyTile]));
-        } else {
-          for (int wv = 0; wv < nwaves; ++wv) sum += colbuf[wv * kKeyTile + threadIdx.x];
-        }
-        if (j < c1) a.A[(size_t)bg * a.max_len + j] = sum;
+    const int t1 = t0 + kKeyTile;
+    if (t1 < c1) {
+      lds_barrier();  // every wave is done reading tile0
+      if (t1 + kKeyTile < c1) {
+        issue_tile<CPR, NW>(kbase, kRowBytes, t1 + kKeyTile, c1, tile0, wave, lane);
+        wait_vm<IPW>();
+      } else {
+        wait_vm<0>();
       }
+      lds_barrier();  // tile1 holds keys [t1, t1+64)
+      score_tile<In, KSTEPS, NW, COLSUM>(a, tile1, qf, qlds, colbuf, sl, t1, c1, interior_of(t1), bg, wave, lane,
+                                         wave_has_rows);
     }
   }
 
@@ -231,17 +370,18 @@ __global__ __launch_bounds__(512) void score_pass(ScoreArgs a) {
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float m = rm[rb][e], z = rz[rb][e];
+        float m = sl.rm[rb][e], z = sl.rz[rb][e];
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) {
           float m2 = __shfl_xor(m, o), z2 = __shfl_xor(z, o);
           float mn = fmaxf(m, m2);
           if (mn != -INFINITY) {
-            z = z * __expf(m - mn) + z2 * __expf(m2 - mn);
+            z = z * exp2f(m - mn) + z2 * exp2f(m2 - mn);
             m = mn;
           }
         }
-        if (l16 == 0) st_out[wave * 32 + rb * 16 + lg * 4 + e] = make_float2(m, z);
+        const int rho = wave * 32 + rb * 16 + lg * 4 + e;
+        if (l16 == 0 && rho < a.rows_pad) st_out[rho] = make_float2(m, z);
       }
   }
 }
@@ -257,12 +397,13 @@ struct ReduceArgs {
   int rows_pad, n_kchunks;
 };
 
-// Row max m over every chunk and the normaliser.  The reference c is 0 when the
-// max lies in [-20, 64] (then exp(z) is taken directly, keeping the full fp32
-// accuracy of small logits), otherwise c = m; inv = 1 / sum_j exp(z_j - c),
-// accumulated in fp64.  Eight lanes share a row (chunks strided by 8) and
-// combine with in-wave shuffles; block 0 of each group also resets the
-// group's selection scratch.
+// Row max m over every chunk and the normaliser, in log2 units (the stats
+// pass keeps m2 = max y and sum 2^(y - m2) with y = z*log2(e)).  The reference
+// c2 is 0 when the natural-log max lies in [-20, 64] (then 2^y is taken
+// directly, keeping the full fp32 accuracy of small logits), otherwise
+// c2 = m2; inv = 1 / sum_j 2^(y_j - c2), accumulated in fp64.  Eight lanes
+// share a row (chunks strided by 8) and combine with in-wave shuffles; block 0
+// of each group also resets the group's selection scratch.
 constexpr int kReduceLanes = 8;
 __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
   const int bg = blockIdx.y, b = bg / a.Hkv;
@@ -278,7 +419,7 @@ __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
     if (m != -INFINITY) {
       for (int c = sub; c < a.n_kchunks; c += kReduceLanes) {
         float2 v = st[(size_t)c * a.rows_pad + rho];
-        if (v.x != -INFINITY) z += (double)v.y * exp((double)v.x - (double)m);
+        if (v.x != -INFINITY) z += (double)v.y * exp2((double)v.x - (double)m);
       }
     }
 #pragma unroll
@@ -286,9 +427,10 @@ __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
     if (sub == 0) {
       float2 ref = make_float2(0.f, 0.f);
       if (m != -INFINITY) {
-        if (m >= -20.f && m <= 64.f) {
+        const double m_nat = (double)m * 0.69314718055994530942;
+        if (m_nat >= -20.0 && m_nat <= 64.0) {
           ref.x = 0.f;
-          ref.y = (float)(1.0 / (z * exp((double)m)));
+          ref.y = (float)(1.0 / (z * exp2((double)m)));
         } else {
           ref.x = m;
           ref.y = (float)(1.0 / z);
@@ -612,43 +754,44 @@ __device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff
   return m < keff ? sel[m] : -1;
 }
 
+// Copy 8 elements (16 bytes of bf16, 32 of fp32) of an input row into the
+// cache, quantising to E4M3 codes of x / scale when the cache is fp8; a NULL
+// source writes zeros.
 template <typename In, typename Out>
-__device__ __forceinline__ void copy_row(const In* src, Out* dst, int width, float inv_scale_unused, float scale,
-                                         int tid, int nthr) {
-  (void)inv_scale_unused;
+__device__ __forceinline__ void copy8(const In* src, Out* dst, float scale) {
   if constexpr (sizeof(Out) == 1) {
-    // quantise 8 elements per step (In = bf16 or fp32)
-    for (int c = tid; c < width / 8; c += nthr) {
-      float f[8];
-      if constexpr (sizeof(In) == 2) {
-        u32x4 raw = src ? *(const u32x4*)(src + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    float f[8];
+    if constexpr (sizeof(In) == 2) {
+      u32x4 raw = src ? *(const u32x4*)src : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          f[2 * i] = bf16_bits_to_f32(raw[i] & 0xffffu);
-          f[2 * i + 1] = bf16_bits_to_f32(raw[i] >> 16);
-        }
-      } else {
-        for (int i = 0; i < 8; ++i) f[i] = src ? ((const float*)src)[c * 8 + i] : 0.f;
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = bf16_bits_to_f32(raw[i] & 0xffffu);
+        f[2 * i + 1] = bf16_bits_to_f32(raw[i] >> 16);
       }
-      u32x2 o;
+    } else {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        uint32_t w = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(f[h * 4 + i] / scale) << (8 * i);
-        o[h] = w;
-      }
-      *(u32x2*)((uint8_t*)dst + c * 8) = o;
+      for (int i = 0; i < 8; ++i) f[i] = src ? src[i] : 0.f;
     }
+    u32x2 o;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(f[h * 4 + i] / scale) << (8 * i);
+      o[h] = w;
+    }
+    *(u32x2*)dst = o;
+  } else if constexpr (sizeof(In) == 2) {
+    *(u32x4*)dst = src ? *(const u32x4*)src : u32x4{0u, 0u, 0u, 0u};
   } else {
-    constexpr int per = 16 / sizeof(In);
-    for (int c = tid; c < width / per; c += nthr) {
-      u32x4 raw = src ? *(const u32x4*)(src + c * per) : u32x4{0u, 0u, 0u, 0u};
-      *(u32x4*)(dst + c * per) = raw;
-    }
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    *(u32x4*)dst = src ? *(const u32x4*)src : z;
+    *(u32x4*)((float*)dst + 4) = src ? *(const u32x4*)(src + 4) : z;
   }
 }
 
+// Each workgroup rewrites rows_per_block cache rows of one (sequence, KV
+// head); threads walk (row, 8-element piece) pairs so every lane copies.
 template <typename In, typename Out>
 __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const int bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
@@ -676,15 +819,18 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const size_t out_row0 = ((size_t)slot * a.Hkv + g) * (size_t)B;
   const float ks = (sizeof(Out) == 1) ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
   const float vs = (sizeof(Out) == 1 && a.v) ? a.v_scale[(size_t)slot * a.Hkv + g] : 1.f;
-  // one wave per row at a time
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  for (int row = row0 + wave; row < row1; row += nw) {
-    int t = row_source(row, L, s, r, keff, sg);
-    const In* ksrc = t >= 0 ? (const In*)a.k + (in_row0 + t) * a.dk : nullptr;
-    copy_row<In, Out>(ksrc, (Out*)a.ck + (out_row0 + row) * a.dk, a.dk, 0.f, ks, lane, 64);
-    if (a.v) {
-      const In* vsrc = t >= 0 ? (const In*)a.v + (in_row0 + t) * a.dv : nullptr;
-      copy_row<In, Out>(vsrc, (Out*)a.cv + (out_row0 + row) * a.dv, a.dv, 0.f, vs, lane, 64);
+  const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
+  const int items = (row1 - row0) * per_row;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int row = row0 + it / per_row, piece = it % per_row;
+    const int t = row_source(row, L, s, r, keff, sg);
+    if (piece < kp) {
+      const In* src = t >= 0 ? (const In*)a.k + (in_row0 + t) * a.dk + 8 * piece : nullptr;
+      copy8<In, Out>(src, (Out*)a.ck + (out_row0 + row) * a.dk + 8 * piece, ks);
+    } else {
+      const int pv = piece - kp;
+      const In* src = t >= 0 ? (const In*)a.v + (in_row0 + t) * a.dv + 8 * pv : nullptr;
+      copy8<In, Out>(src, (Out*)a.cv + (out_row0 + row) * a.dv + 8 * pv, vs);
     }
   }
 }
@@ -732,36 +878,32 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   return g;
 }
 
+template <typename In, int KS, int NW>
+static hipError_t launch_score_nw(const ScoreArgs& sa, bool colsum, int groups, int n_kchunks, hipStream_t st) {
+  dim3 grid(n_kchunks, groups), block(64 * NW);
+  if (colsum)
+    hipLaunchKernelGGL((score_pass<In, KS, NW, true>), grid, block, 0, st, sa);
+  else
+    hipLaunchKernelGGL((score_pass<In, KS, NW, false>), grid, block, 0, st, sa);
+  return hipGetLastError();
+}
+
+// Waves per workgroup: 4 while the score rows fit in 128, else 8.
 template <typename In>
-static hipError_t launch_score(const ScoreArgs& sa, int dk, int nwaves, bool colsum, int groups, int n_kchunks,
-                               hipStream_t st) {
-  dim3 grid(n_kchunks, groups);
-  dim3 block(64 * nwaves);
-  size_t pitch = (size_t)dk * sizeof(In) + 16;
-  size_t lds = kKeyTile * pitch + 8 * kKeyTile * sizeof(float);
-  if (sizeof(In) == 4) lds += (size_t)sa.rows_pad * dk * sizeof(float);
-#define SNAP_SCORE(KS)                                                                        \
-  if (dk == KS * 32) {                                                                        \
-    const void* fn = colsum ? (const void*)score_pass<In, KS, true> : (const void*)score_pass<In, KS, false>; \
-    if (lds > 65536) {                                                                        \
-      hipError_t ae = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
-      if (ae != hipSuccess) return ae;                                                        \
-    }                                                                                         \
-    if (colsum)                                                                               \
-      hipLaunchKernelGGL((score_pass<In, KS, true>), grid, block, lds, st, sa);               \
-    else                                                                                      \
-      hipLaunchKernelGGL((score_pass<In, KS, false>), grid, block, lds, st, sa);              \
-    return hipGetLastError();                                                                 \
-  }
+static hipError_t launch_score(const ScoreArgs& sa, int dk, bool colsum, int groups, int n_kchunks, hipStream_t st) {
+  const bool wide = sa.rows_pad > 128;
   if constexpr (sizeof(In) == 2) {
-    SNAP_SCORE(2)
-    SNAP_SCORE(4)
-    SNAP_SCORE(18)
+    if (dk == 64) return wide ? launch_score_nw<In, 2, 8>(sa, colsum, groups, n_kchunks, st)
+                              : launch_score_nw<In, 2, 4>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 128) return wide ? launch_score_nw<In, 4, 8>(sa, colsum, groups, n_kchunks, st)
+                               : launch_score_nw<In, 4, 4>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 576) return wide ? launch_score_nw<In, 18, 8>(sa, colsum, groups, n_kchunks, st)
+                               : launch_score_nw<In, 18, 4>(sa, colsum, groups, n_kchunks, st);
   } else {
-    SNAP_SCORE(2)
-    SNAP_SCORE(4)
+    if (wide) return hipErrorInvalidValue;  // fp32 inputs: at most 128 score rows
+    if (dk == 64) return launch_score_nw<In, 2, 4>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 128) return launch_score_nw<In, 4, 4>(sa, colsum, groups, n_kchunks, st);
   }
-#undef SNAP_SCORE
   return hipErrorInvalidValue;
 }
 
@@ -803,12 +945,13 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   sa.key_chunk = geo.key_chunk;
   sa.n_kchunks = geo.n_kchunks;
   sa.scale = scale;
-  const int nwaves = geo.rows_pad / 32;
+  sa.scale2 = (float)((double)scale * 1.4426950408889634074);
+  sa.scale2_lo = (float)((double)scale * 1.4426950408889634074 - (double)sa.scale2);
   const bool bf = p.in_dtype == SNAP_BF16;
   hipError_t e;
 
-  e = bf ? launch_score<uint16_t>(sa, p.d_qk, nwaves, false, groups, geo.n_kchunks, stream)
-         : launch_score<float>(sa, p.d_qk, nwaves, false, groups, geo.n_kchunks, stream);
+  e = bf ? launch_score<uint16_t>(sa, p.d_qk, false, groups, geo.n_kchunks, stream)
+         : launch_score<float>(sa, p.d_qk, false, groups, geo.n_kchunks, stream);
   if (e != hipSuccess) return SNAP_ERR_HIP;
 
   ReduceArgs ra;
@@ -828,8 +971,8 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + 31) / 32, groups), dim3(256), 0, stream, ra);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
 
-  e = bf ? launch_score<uint16_t>(sa, p.d_qk, nwaves, true, groups, geo.n_kchunks, stream)
-         : launch_score<float>(sa, p.d_qk, nwaves, true, groups, geo.n_kchunks, stream);
+  e = bf ? launch_score<uint16_t>(sa, p.d_qk, true, groups, geo.n_kchunks, stream)
+         : launch_score<float>(sa, p.d_qk, true, groups, geo.n_kchunks, stream);
   if (e != hipSuccess) return SNAP_ERR_HIP;
 
   SelectArgs se;
