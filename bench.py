@@ -35,6 +35,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--event-every", type=int, default=16, help="time decode calls of every n-th decode step")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -89,6 +91,14 @@ def main():
     t_setup = time.time() - t_setup
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
+
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- one step
     def step(timing):
@@ -146,7 +156,7 @@ def main():
     q_bytes = n * wl.n_q_heads * wl.d_qk * 2
     o_bytes = n * wl.n_q_heads * wl.d_v * 2
     dec_bytes = valid * wl.n_kv_heads * row_bytes + q_bytes + o_bytes
-    dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
+    dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9 if dec_ms > 0 else 0.0
     tokens = n * dsteps
     value = tokens / (ms_step * 1e-3)
     decode_ms_per_token_step = dec_ms * layers  # attention only, per decode step (all layers)
@@ -171,7 +181,7 @@ def main():
                    "kv_dtype": wl.kv_dtype},
         "decode_attn_ms_per_call": round(dec_ms, 4),
         "decode_attn_hbm_gbps": round(dec_gbps, 1),
-        "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1),
+        "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1) if dec_ms > 0 else 0.0,
         "compress_ms_per_layer_call": round(comp_ms, 4),
         "compress_ms_per_seq_layer": round(comp_ms / n, 4),
         "roofline": {"bound": "hbm", "kernel": "snap_decode_attn (split-K partials + combine)",

@@ -18,6 +18,11 @@ def build(verbose: bool = False) -> str:
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
            # packed fp32 VALU ops stay off: plain fp32 math everywhere
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # MFMA results in VGPRs: no per-element accumulator moves
+           "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+           # IEEE mode off: no NaN reaches a min/max (masked lanes hold -inf),
+           # so max needs no operand canonicalisation
+           "-fno-honor-nans", "-mno-amdgpu-ieee",
            "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]

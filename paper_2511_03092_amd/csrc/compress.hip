@@ -118,7 +118,7 @@ __device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c
   const float yh = acc * s2;
   float yl = fmaf(acc, s2, -yh);
   yl = fmaf(acc, s2lo, yl);
-  return exp2f(yh - c) * fmaf(yl, invl, inv);
+  return fast_exp2(yh - c) * fmaf(yl, invl, inv);
 }
 
 // One 64-key tile already resident in LDS: scores for this wave's 32 rows,
@@ -141,54 +141,57 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
   for (int sb = 0; sb < kKeyTile / 16; ++sb) {
     f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
     const int key = sb * 16 + l16;
-    if (wave_has_rows) {
-      if constexpr (kBF16) {
+    if constexpr (kBF16) {
+      // waves without score rows multiply zero fragments (only tiny cases have them)
 #pragma unroll
-        for (int t = 0; t < KSTEPS; ++t) {
-          bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot(key, KSTEPS * lg + t) * 16));
-          acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
-          acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
-        }
-      } else {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
-            // fp32 products are exact in fp64; only the final rounding remains
-            double sacc = 0.0;
-#pragma unroll 4
-            for (int d = 0; d < D; ++d) {
-              const float kd = *(const float*)(ktile + (size_t)tile_slot(key, d >> 2) * 16 + (d & 3) * 4);
-              sacc = fma((double)qrow[d], (double)kd, sacc);
-            }
-            acc[rb][e] = (float)sacc;
-          }
+      for (int t = 0; t < KSTEPS; ++t) {
+        bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot(key, KSTEPS * lg + t) * 16));
+        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
       }
-    }
-    const int j = t0 + key;
-    float colv[2][4];
-    if (interior) {
+    } else if (wave_has_rows) {
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (!COLSUM)
-            xv[rb][e][sb] = acc[rb][e] * s2;
-          else
-            colv[rb][e] = weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]);
+          const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
+          // fp32 products are exact in fp64; only the final rounding remains
+          double sacc = 0.0;
+#pragma unroll 4
+          for (int d = 0; d < D; ++d) {
+            const float kd = *(const float*)(ktile + (size_t)tile_slot(key, d >> 2) * 16 + (d & 3) * 4);
+            sacc = fma((double)qrow[d], (double)kd, sacc);
+          }
+          acc[rb][e] = (float)sacc;
         }
+    }
+    const int j = t0 + key;
+    float colv[2][4];
+    if (!COLSUM) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) xv[rb][e][sb] = acc[rb][e] * s2;
+      if (!interior) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) xv[rb][e][sb] = -INFINITY;
+      }
     } else {
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool in = sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e];
-          if (!COLSUM)
-            xv[rb][e][sb] = in ? acc[rb][e] * s2 : -INFINITY;
-          else
-            colv[rb][e] = in ? weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]) : 0.f;
-        }
+        for (int e = 0; e < 4; ++e)
+          colv[rb][e] = weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]);
+      if (!interior) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) colv[rb][e] = 0.f;
+      }
     }
     if (COLSUM) {
       float cs = ((colv[0][0] + colv[0][1]) + (colv[0][2] + colv[0][3])) +
@@ -206,8 +209,8 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
         float mt = fmaxf(fmaxf(xv[rb][e][0], xv[rb][e][1]), fmaxf(xv[rb][e][2], xv[rb][e][3]));
         float mn = fmaxf(sl.rm[rb][e], mt);
         if (mn == -INFINITY) continue;
-        float z = sl.rz[rb][e] * exp2f(sl.rm[rb][e] - mn);
-        z += (exp2f(xv[rb][e][0] - mn) + exp2f(xv[rb][e][1] - mn)) + (exp2f(xv[rb][e][2] - mn) + exp2f(xv[rb][e][3] - mn));
+        float z = sl.rz[rb][e] * fast_exp2(sl.rm[rb][e] - mn);
+        z += (fast_exp2(xv[rb][e][0] - mn) + fast_exp2(xv[rb][e][1] - mn)) + (fast_exp2(xv[rb][e][2] - mn) + fast_exp2(xv[rb][e][3] - mn));
         sl.rz[rb][e] = z;
         sl.rm[rb][e] = mn;
       }
@@ -376,7 +379,7 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
           float m2 = __shfl_xor(m, o), z2 = __shfl_xor(z, o);
           float mn = fmaxf(m, m2);
           if (mn != -INFINITY) {
-            z = z * exp2f(m - mn) + z2 * exp2f(m2 - mn);
+            z = z * fast_exp2(m - mn) + z2 * fast_exp2(m2 - mn);
             m = mn;
           }
         }
@@ -528,7 +531,7 @@ __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
   if (a.pooled_out && split == 0) {
     float* po = a.pooled_out + (size_t)bg * a.max_len;
     for (int j = threadIdx.x; j < a.max_len; j += blockDim.x)
-      if (j < c0 || j >= c1) po[j] = __builtin_nanf("");
+      if (j < c0 || j >= c1) po[j] = __uint_as_float(kQuietNaN);
   }
   if (st.mode == 2) clear_hists(lhist);
   if (j0 < j1) {

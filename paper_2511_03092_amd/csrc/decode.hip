@@ -195,9 +195,9 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) pe[i] = 0.f;
     } else {
-      alpha = exp2f(m - mn);
+      alpha = fast_exp2(m - mn);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = exp2f(x[i] - mn);
+      for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(x[i] - mn);
     }
     m = mn;
     lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
@@ -348,9 +348,9 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) pe[i] = 0.f;
     } else {
-      alpha = exp2f(m - mn);
+      alpha = fast_exp2(m - mn);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = exp2f(x[i] - mn);
+      for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(x[i] - mn);
     }
     m = mn;
     lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
@@ -446,8 +446,8 @@ __global__ __launch_bounds__(64) void decode_generic(DecodeArgs a) {
     dot = warp_sum(dot);
     const float x = dot * xs;
     const float mn = fmaxf(m, x);
-    const float alpha = exp2f(m - mn);
-    const float pe = exp2f(x - mn);
+    const float alpha = fast_exp2(m - mn);
+    const float pe = fast_exp2(x - mn);
     lsum = lsum * alpha + pe;
     m = mn;
 #pragma unroll
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   float ws = 0.f;
   for (int c = threadIdx.x; c < a.n_chunks; c += blockDim.x) {
     float2 v = ml[c];
-    float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : exp2f(v.x - M);
+    float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : fast_exp2(v.x - M);
     wts[c] = wc;
     ws += wc * v.y;
   }

@@ -12,6 +12,7 @@
 namespace snap {
 
 constexpr int kWave = 64;
+constexpr uint32_t kQuietNaN = 0x7fc00000u;  // written as bits: kernels build without NaN semantics
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -51,9 +52,14 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
 __device__ __forceinline__ float e4m3_to_f32(uint32_t c) {
   uint32_t cm = c & 0x7fu;
   float mag = (cm < 8u) ? (float)cm * (1.0f / 512.0f) : __uint_as_float((cm << 20) + (120u << 23));
-  if (cm == 0x7fu) mag = __builtin_nanf("");
+  if (cm == 0x7fu) mag = __uint_as_float(0x7fc00000u);  // the E4M3 NaN code
   return (c & 0x80u) ? -mag : mag;
 }
+
+// 2^x by the hardware instruction (about 1 ulp).  Results below 2^-126 flush
+// to zero; every caller exponentiates a value relative to a running maximum,
+// where such terms are negligible.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ float warp_sum(float v) {
 #pragma unroll
