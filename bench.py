@@ -21,6 +21,22 @@ import sys
 import time
 
 DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per decode-attention call from the committed counter runs
+    (profiles/traffic.json), or None when no record exists or the decode
+    kernels have changed since the counters were taken."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(HERE, "profiles", "traffic.json")))[workload]
+        src = open(os.path.join(HERE, "paper_2511_03092_amd", "csrc", "decode.hip"), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec.get("decode_source_sha256"):
+        return None
+    return rec["traffic_bytes_per_launch"]
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 
@@ -186,7 +202,7 @@ def main():
         "compress_ms_per_seq_layer": round(comp_ms / n, 4),
         "roofline": {"bound": "hbm", "kernel": "snap_decode_attn (split-K partials + combine)",
                      "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(wl.name),
                      "algorithmic_bytes_per_launch": dec_bytes},
         "setup_s": round(t_setup, 1),
     }
