@@ -396,6 +396,209 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- latent decode, LDS-staged
+// bf16 latent caches (576-wide rows, values = first 512 dims).  One workgroup
+// of 4 waves per (chunk, sequence) streams blocks of 32 rows through a
+// kLatStages-deep ring of LDS stages with direct global->LDS loads, so about
+// three blocks (110 KB) are in flight per CU while one is consumed.  Wave w
+// computes partial logits over its share of the 18 k-steps (5,5,4,4), the
+// four partials are summed through LDS in a fixed order, and wave w computes
+// the value product for dims [128w, 128w+128).
+// LDS rows are 72 chunks of 16 bytes; chunk c of row r sits at slot
+// r*72 + (c ^ ((r >> 1) & 7)), which makes both the key-fragment reads (one
+// chunk of 16 consecutive rows) and the value reads (16 consecutive chunks of
+// one row) free of bank conflicts.
+constexpr int kLatStages = 4;
+constexpr int kLatRowBytes = 576 * 2;
+constexpr int kLatChunks = kLatRowBytes / 16;        // 72
+constexpr int kLatBlockBytes = 32 * kLatRowBytes;    // 36864
+constexpr int kLatLoadsPerWave = 32 * kLatChunks / 64 / 4;  // 9 wave-instructions per block per wave
+
+__device__ __forceinline__ int lat_slot(int r, int c) { return r * kLatChunks + (c ^ ((r >> 1) & 7)); }
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr_t;
+// One wave-instruction of global -> LDS copy (lane i's 16 bytes land at
+// lds_wave_base + 16*i), issued through inline asm so that the only ordering
+// with later LDS reads is the caller's explicit vmcnt wait and barrier.  M0
+// (the DMA's LDS base) is saved and restored around it.
+__device__ __forceinline__ void dma16_lat(const void* g, const void* lds_wave_base) {
+  const uint32_t la = (uint32_t)(uintptr_t)(lds_void_ptr_t)lds_wave_base;
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(la), "v"(g)
+      : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void lat_wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void lat_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
+  constexpr int D = 576;
+  __shared__ __align__(16) unsigned char stage[kLatStages][kLatBlockBytes];
+  __shared__ f32x4 sx[4][2][64];  // partial logits [wave][row set][lane]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  int slot;
+  RowSpan sp;
+  if (!span_of(a, b, chunk, slot, sp)) return;
+  const int sr = a.sink + a.recent;
+  const int B = sr + a.topk;
+  const int h = l16;
+  const bool hval = h < a.G;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+
+  // wave w owns k-steps [kb, kb+kc) of the 18 (5,5,4,4); lane group lg holds
+  // dims 32*kb + 8*(kc*lg + t), t < kc
+  const int kb = mla_kbeg(wu), kc = mla_kcnt(wu);
+  bf16x8 qf[5];
+  {
+    const uint16_t* qp = (const uint16_t*)a.q + ((size_t)b * a.Hq + (hval ? h : 0)) * D;
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (hval && t < kc) v = *(const u32x4*)(qp + 32 * kb + 8 * (kc * lg + t));
+      qf[t] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  // this lane's share of every block load: (row, chunk) of its 9 slots
+  int ld_r[kLatLoadsPerWave], ld_c[kLatLoadsPerWave];
+#pragma unroll
+  for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
+    const int q = (wu + 4 * ii) * 64 + lane;
+    const int r = q / kLatChunks, cs = q % kLatChunks;
+    ld_r[ii] = r;
+    ld_c[ii] = cs ^ ((r >> 1) & 7);
+  }
+  const unsigned char* cache = (const unsigned char*)a.ck + (size_t)slot * B * kLatRowBytes;
+  const int nblk = (sp.v1 - sp.v0 + 31) / 32;
+  auto issue = [&](int blk) {
+    const int vb = sp.v0 + 32 * blk;
+    unsigned char* dst = &stage[blk % kLatStages][0];
+#pragma unroll
+    for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
+      int v = vb + ld_r[ii];
+      v = v < sp.v1 ? v : sp.v1 - 1;
+      const unsigned char* src = cache + (size_t)virt_row(v, sp.n1, sr) * kLatRowBytes + ld_c[ii] * 16;
+      dma16_lat(src, dst + (size_t)(wu + 4 * ii) * 1024);
+    }
+  };
+
+  const float xs = a.scale * kLog2e;
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  lat_wait_vm<0>();  // query fragments landed; from here vmcnt counts block loads only
+  for (int s = 0; s < kLatStages && s < nblk; ++s) issue(s);
+
+  for (int i = 0; i < nblk; ++i) {
+    const int after = min(nblk - 1 - i, kLatStages - 1);  // block loads issued after block i
+    if (after >= 3)
+      lat_wait_vm<3 * kLatLoadsPerWave>();
+    else if (after == 2)
+      lat_wait_vm<2 * kLatLoadsPerWave>();
+    else if (after == 1)
+      lat_wait_vm<kLatLoadsPerWave>();
+    else
+      lat_wait_vm<0>();
+    lat_barrier();  // block i is in LDS for every wave
+    const unsigned char* st = &stage[i % kLatStages][0];
+    const int vb = sp.v0 + 32 * i;
+
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      if (t < kc) {
+        const int c = 4 * kb + kc * lg + t;
+        const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(l16, c) * 16));
+        const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(16 + l16, c) * 16));
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[t], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[t], s1, 0, 0, 0);
+      }
+    }
+    // sum the four waves' partial logits in a fixed order (identical in every wave)
+    sx[w][0][lane] = s0;
+    sx[w][1][lane] = s1;
+    lat_barrier();
+    s0 = ((sx[0][0][lane] + sx[1][0][lane]) + sx[2][0][lane]) + sx[3][0][lane];
+    s1 = ((sx[0][1][lane] + sx[1][1][lane]) + sx[2][1][lane]) + sx[3][1][lane];
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
+      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+    }
+    float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float mn = fmaxf(m, bm);
+    float alpha = 1.f, pe[8];
+    if (mn == -INFINITY) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) pe[k] = 0.f;
+    } else {
+      alpha = fast_exp2(m - mn);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) pe[k] = fast_exp2(x[k] - mn);
+    }
+    m = mn;
+    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    u32x4 pw;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pw[k] = f32_to_bf16_bits(pe[2 * k]) | (f32_to_bf16_bits(pe[2 * k + 1]) << 16);
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+    u32x4 vv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int r = k < 4 ? 4 * lg + k : 16 + 4 * lg + (k - 4);
+      vv[k] = *(const u32x4*)(st + (size_t)lat_slot(r, 16 * w + l16) * 16);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int u = c >> 1;
+      const uint32_t selb = (c & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 av;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) av[k] = __builtin_amdgcn_perm(vv[2 * k + 1][u], vv[2 * k][u], selb);
+      acc[c] *= alpha;
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[c], 0, 0, 0);
+    }
+    lat_barrier();  // every wave is done with this stage
+    if (i + kLatStages < nblk) issue(i + kLatStages);
+  }
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (!hval) return;
+  const size_t pi = ((size_t)b * a.Hq + h) * a.n_chunks + chunk;
+  if (w == 0 && lg == 0) a.ml[pi] = make_float2(m, lsum);
+  float* dst = a.part + pi * a.dv + 128 * w;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float4 lo = make_float4(acc[0][e], acc[1][e], acc[2][e], acc[3][e]);
+    float4 hi = make_float4(acc[4][e], acc[5][e], acc[6][e], acc[7][e]);
+    float* d = dst + 8 * (4 * lg + e);
+    *(float4*)d = lo;
+    *(float4*)(d + 4) = hi;
+  }
+}
+
 // ---------------------------------------------------------------- generic decode
 template <typename KV>
 __device__ __forceinline__ float load_kv(const void* base, size_t i, float scale) {
@@ -617,7 +820,8 @@ Geometry decode_geometry(const snap_params& p, int n) {
   const int units = (n > 0 ? n : 1) * p.n_kv_heads;
   // latent caches run 4-wave workgroups (two per CU), the others one wave each
   const bool latent = p.v_in_k && p.d_qk == 576;
-  const int target = latent ? 512 : 2048;
+  const bool latent_lds = latent && p.kv_dtype == SNAP_BF16;  // one 4-wave workgroup per CU (LDS-bound)
+  const int target = latent_lds ? 256 : (latent ? 512 : 2048);
   const int min_rows = latent ? 256 : 128;
   int want = (target + units - 1) / units;
   int maxc = (B + min_rows - 1) / min_rows;
@@ -670,7 +874,7 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
     if (p.kv_dtype == SNAP_FP8_E4M3)
       hipLaunchKernelGGL((decode_mla<true>), grid, dim3(256), 0, stream, a);
     else
-      hipLaunchKernelGGL((decode_mla<false>), grid, dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(decode_mla_lds, grid, dim3(256), 0, stream, a);
   } else if (mfma_ok) {
     dim3 grid(geo.n_chunks, n * p.n_kv_heads);
     if (p.kv_dtype == SNAP_FP8_E4M3)
