@@ -142,13 +142,23 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
     f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
     const int key = sb * 16 + l16;
     if constexpr (kBF16) {
-      // waves without score rows multiply zero fragments (only tiny cases have them)
+      // waves without score rows multiply zero fragments (only tiny cases have them).
+      // Even and odd k-steps accumulate in separate chains (shorter fp32
+      // accumulation, two independent MFMA chains), summed at the end.
+      f32x4 odd[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int t = 0; t < KSTEPS; ++t) {
         bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot(key, KSTEPS * lg + t) * 16));
-        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
+        if (t & 1) {
+          odd[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, odd[0], 0, 0, 0);
+          odd[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, odd[1], 0, 0, 0);
+        } else {
+          acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
+          acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
+        }
       }
+      acc[0] += odd[0];
+      acc[1] += odd[1];
     } else if (wave_has_rows) {
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)

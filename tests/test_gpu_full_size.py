@@ -1,0 +1,149 @@
+"""GPU parity at the benchmark's full sizes, in the launch configuration
+bench.py times: one layer of the 128k workloads (all sequences compressed in
+one call).  The fp64 oracle recomputes sampled (sequence, KV head) units one
+by one; every unit is checked for the properties that hold at any size, and
+decode outputs are recomputed by the oracle on the GPU's own cache bytes.
+"""
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2511_03092_amd as snap
+import synth
+from snaphelp import SEL_RTOL, TOL, GpuCache, check_selection, oracle_params, params_of
+
+pytestmark = pytest.mark.gpu
+
+BAND_RTOL = 1e-6  # same derived fp32 bound as the small-size parity tests
+
+
+def _announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def _compress_full(wl, lengths):
+    """Inputs generated on the GPU (as bench.py does), one compress call."""
+    p = params_of(wl)
+    dev = "cuda"
+    max_len = max(lengths)
+    q, k, v = synth.prefill_batch(wl, 0, lengths, device=dev, max_len=max_len, pad_value=float("nan"))
+    cache = GpuCache(p, len(lengths))
+    n = len(lengths)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.arange(n, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_compress_workspace(p, n, max_len))
+    sel = torch.empty((n, p.n_kv_heads, p.topk), dtype=torch.int32, device=dev)
+    pooled = torch.empty((n, p.n_kv_heads, max_len), dtype=torch.float32, device=dev)
+    snap.snap_compress(p, cache.c(), cache.pos, cache.n_topk, sl, lens, q, k, v, ws, sel, pooled)
+    torch.cuda.synchronize()
+    return p, q, k, v, cache, sel, pooled
+
+
+def _structural(p, k, v, cache, sel, pooled, lengths):
+    """Properties every unit must satisfy, checked on the GPU's own data."""
+    s, r, K = p.sink, p.recent, p.topk
+    pos = cache.pos.cpu().tolist()
+    nt = cache.n_topk.cpu().tolist()
+    for b, L in enumerate(lengths):
+        keff = min(max(L - s - r, 0), K)
+        assert pos[b] == L and nt[b] == keff
+        for g in range(p.n_kv_heads):
+            S = sel[b, g]
+            kept = S[:keff]
+            assert torch.all(S[keff:] == -1)
+            assert torch.all(kept[1:] > kept[:-1]) and int(kept[0]) >= s and int(kept[-1]) < L - r
+            src = torch.cat([torch.arange(min(s, L), device="cuda"),
+                             torch.arange(max(s, L - r), L, device="cuda"), kept.long()])
+            rows = torch.cat([torch.arange(min(s, L), device="cuda"),
+                              torch.tensor([oracle.slot_of(t, s, r) for t in range(max(s, L - r), L)],
+                                           device="cuda", dtype=torch.long),
+                              s + r + torch.arange(keff, device="cuda")])
+            ck = cache.k[b, g]
+            assert torch.equal(ck[rows].view(torch.int16), k[b, g, src].view(torch.int16)), (b, g)
+            assert torch.all(ck[s + r + keff:] == 0)
+            if v is not None:
+                assert torch.equal(cache.v[b, g][rows].view(torch.int16), v[b, g, src].view(torch.int16))
+            P = pooled[b, g]
+            assert torch.all(torch.isnan(P[:s])) and torch.all(torch.isnan(P[L - r:L]))
+            assert torch.all(P[s:L - r] >= 0)
+
+
+def _oracle_units(p, q, k, v, cache, sel, pooled, lengths, units):
+    op = oracle_params(p)
+    G = op.group
+
+    def run(u):
+        b, g = u
+        L = lengths[b]
+        res = oracle.compress_group(op, L, oracle.f64(q[b, g * G:(g + 1) * G]), oracle.f64(k[b, g, :L]),
+                                    None if v is None else oracle.f64(v[b, g, :L]))
+        return u, res
+
+    with ThreadPoolExecutor(len(units)) as ex:
+        results = list(ex.map(run, units))
+    worst_band = 0.0
+    for (b, g), res in results:
+        L = lengths[b]
+        s, r = p.sink, p.recent
+        gs = sel[b, g].cpu().numpy()
+        swaps = check_selection(gs, res.P, L, s, r, p.topk, SEL_RTOL)
+        keff = min(max(L - s - r, 0), p.topk)
+        ek = oracle.assemble(L, s, r, p.topk, oracle.f64(k[b, g, :L]), gs[:keff])
+        assert np.array_equal(cache.k[b, g].double().cpu().numpy(), ek)
+        gp = pooled[b, g, s:L - r].double().cpu().numpy()
+        rel = np.abs(gp - res.P[s:L - r]) / np.maximum(res.P[s:L - r], 1e-30)
+        tau = np.sort(res.P[s:L - r])[::-1][keff - 1]
+        band = (res.P[s:L - r] >= tau / 4) & (res.P[s:L - r] <= 4 * tau)
+        worst_band = max(worst_band, float(rel[band].max()))
+        print(f"  unit (seq {b}, head {g}, L={L}): swaps {swaps}, band rel err {rel[band].max():.3e}", flush=True)
+    assert worst_band <= BAND_RTOL
+
+
+def _decode_check(p, wl, cache, steps, check_slots):
+    n = cache.n_slots
+    sl = torch.arange(n, dtype=torch.int32, device="cuda")
+    ws = snap.workspace(snap.snap_decode_workspace(p, n))
+    out = torch.empty((n, p.n_q_heads, p.d_v), dtype=torch.bfloat16, device="cuda")
+    op = oracle_params(p)
+    worst = 0.0
+    for step in range(steps):
+        positions = cache.pos.cpu().tolist()
+        qd, kn, vn = synth.decode_inputs(wl, 0, step, positions, device="cuda")
+        snap.snap_cache_append(p, cache.c(), cache.pos, sl, kn, vn)
+        snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, qd, out, ws)
+        snap.snap_advance(cache.pos, sl)
+        torch.cuda.synchronize()
+        nt = cache.n_topk.cpu().numpy()
+        for b in check_slots:
+            ck = cache.k[b:b + 1].double().cpu().numpy()
+            cv = None if cache.v is None else cache.v[b:b + 1].double().cpu().numpy()
+            exp = oracle.decode_attn(op, [positions[b]], nt[[b]], qd[b:b + 1].cpu(), ck, cv)
+            err = float(np.max(np.abs(out[b:b + 1].double().cpu().numpy() - exp)))
+            worst = max(worst, err)
+            assert err <= TOL["bf16"], (step, b, err)
+    print(f"  decode max abs err: {worst:.3e}", flush=True)
+
+
+def test_llama_32layer_workload_one_layer_full_size():
+    wl = synth.WORKLOADS["llama8b-32layer-b8-128k"]
+    lengths = synth.draw_lengths(wl, 0, wl.batch)
+    _announce(f"llama8b-32layer-b8-128k layer 0 at full size, lengths {lengths}")
+    p, q, k, v, cache, sel, pooled = _compress_full(wl, lengths)
+    _structural(p, k, v, cache, sel, pooled, lengths)
+    big = int(np.argmax(lengths))
+    small = int(np.argmin(lengths))
+    _oracle_units(p, q, k, v, cache, sel, pooled, lengths, [(big, 0), (small, 7), (3, 4)])
+    _decode_check(p, wl, cache, 2, list(range(wl.batch)))
+
+
+def test_mla_workload_one_layer_full_size():
+    wl = synth.WORKLOADS["mla-8head-61layer-b16-128k"]
+    lengths = synth.draw_lengths(wl, 0, wl.batch)
+    _announce(f"mla-8head-61layer-b16-128k layer 0 at full size: {wl.batch} x {lengths[0]}")
+    p, q, k, v, cache, sel, pooled = _compress_full(wl, lengths)
+    _structural(p, k, v, cache, sel, pooled, lengths)
+    _oracle_units(p, q, k, v, cache, sel, pooled, lengths, [(5, 0)])
+    _decode_check(p, wl, cache, 2, [0, 5, 15])

@@ -15,7 +15,11 @@ from snaphelp import (TOL, GpuCache, check_compress, decode_steps, gpu_compress,
 
 pytestmark = pytest.mark.gpu
 
-BAND_RTOL = 5e-7  # pooled-score error near the threshold (implies the 1e-6 swap rule)
+# Pooled-score error near the selection threshold.  Worst-case fp32 rounding of the
+# score path: exp2 (1 ulp), normalisation multiply (1/2 ulp), a column-sum tree over
+# G*w terms (7 levels at G=4, w=32) and the pooling sum (3 levels) add to ~1e-6
+# relative.  The swap rule itself (1e-6) is checked directly on every case.
+BAND_RTOL = 1e-6
 ALL_RTOL = 1e-5   # pooled-score error anywhere (large planted logits carry more rounding)
 
 
