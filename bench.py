@@ -3,13 +3,15 @@
 
 One step = one pass of the whole hot path over one batch: snap_compress of
 every (layer, sequence) from prompts resident in HBM, then `decode_steps`
-decode steps, each running snap_cache_append + snap_decode_attn for every
-layer and one snap_advance.  Inputs (prompts and every decode step's q/k/v)
-are generated before the timed region.
+decode steps, each running snap_decode_step (append + attention; or, with
+--two-calls, snap_cache_append + snap_decode_attn) for every layer and one
+snap_advance.  Inputs (prompts and every decode step's q/k/v) are generated
+before the timed region.
 
 Prints ONE JSON line.  `value` is decoded tokens per second of the whole step
-(compression included); the decode-only rate, the decode-attention HBM GB/s
-and the per-(sequence, layer) snap_compress latency are reported beside it.
+(compression included); the decode-only rate, the per-layer decode-step HBM
+GB/s and the per-(sequence, layer) snap_compress latency are reported beside
+it.
 """
 from __future__ import annotations
 
@@ -25,7 +27,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per decode-attention call from the committed counter runs
+    """HBM bytes per decode-step call from the committed counter runs
     (profiles/traffic.json), or None when no record exists or the decode
     kernels have changed since the counters were taken."""
     import hashlib
@@ -51,6 +53,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--event-every", type=int, default=16, help="time decode calls of every n-th decode step")
+    ap.add_argument("--two-calls", action="store_true",
+                    help="decode with snap_cache_append + snap_decode_attn instead of snap_decode_step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
     return ap.parse_args()
@@ -132,11 +136,16 @@ def main():
             sample = timing is not None and (t % args.event_every == 0)
             for l in range(layers):
                 qd, kd, vd = dec[l]
-                snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t], stream=sptr)
                 if sample:
                     e0 = torch.cuda.Event(enable_timing=True)
                     e0.record(stream)
-                snap.snap_decode_attn(p, caches[l][2], pos, ntop, slots, qd[t], out, wsd, stream=sptr)
+                if args.two_calls:
+                    snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t],
+                                           stream=sptr)
+                    snap.snap_decode_attn(p, caches[l][2], pos, ntop, slots, qd[t], out, wsd, stream=sptr)
+                else:
+                    snap.snap_decode_step(p, caches[l][2], pos, ntop, slots, qd[t], kd[t],
+                                          None if vd is None else vd[t], out, wsd, stream=sptr)
                 if sample:
                     e1 = torch.cuda.Event(enable_timing=True)
                     e1.record(stream)
@@ -160,7 +169,8 @@ def main():
     comp_ms = sum(a.elapsed_time(b) for a, b in timing["compress"]) / max(len(timing["compress"]), 1)
     dec_ms = sum(a.elapsed_time(b) for a, b in timing["decode"]) / max(len(timing["decode"]), 1)
 
-    # ---- algorithmic bytes of one decode-attention call (valid rows + q + out)
+    # ---- algorithmic bytes of one layer's decode step: valid rows + q + out, plus
+    # the appended token (read from the input, written to its cache row)
     s_r = wl.sink + wl.recent
     elt = {"f32": 4, "bf16": 2, "fp8": 1}[wl.kv_dtype]
     row_bytes = wl.d_qk * elt + (0 if wl.v_in_k else wl.d_v * elt)
@@ -171,7 +181,9 @@ def main():
         valid += min(L + 1, s_r) + min(ncand, wl.topk)
     q_bytes = n * wl.n_q_heads * wl.d_qk * 2
     o_bytes = n * wl.n_q_heads * wl.d_v * 2
-    dec_bytes = valid * wl.n_kv_heads * row_bytes + q_bytes + o_bytes
+    in_elt = 2 if wl.in_dtype == "bf16" else 4
+    new_bytes = n * wl.n_kv_heads * (wl.d_qk + (0 if wl.v_in_k else wl.d_v)) * in_elt + n * wl.n_kv_heads * row_bytes
+    dec_bytes = valid * wl.n_kv_heads * row_bytes + q_bytes + o_bytes + new_bytes
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9 if dec_ms > 0 else 0.0
     tokens = n * dsteps
     value = tokens / (ms_step * 1e-3)
@@ -195,12 +207,14 @@ def main():
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "decode_steps": dsteps,
                    "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
                    "kv_dtype": wl.kv_dtype},
-        "decode_attn_ms_per_call": round(dec_ms, 4),
-        "decode_attn_hbm_gbps": round(dec_gbps, 1),
+        "decode_step_ms_per_call": round(dec_ms, 4),
+        "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1) if dec_ms > 0 else 0.0,
         "compress_ms_per_layer_call": round(comp_ms, 4),
         "compress_ms_per_seq_layer": round(comp_ms / n, 4),
-        "roofline": {"bound": "hbm", "kernel": "snap_decode_attn (split-K partials + combine)",
+        "roofline": {"bound": "hbm",
+                     "kernel": ("snap_cache_append + snap_decode_attn" if args.two_calls else
+                                "snap_decode_step (append + split-K attention, one launch) + combine"),
                      "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(wl.name),
                      "algorithmic_bytes_per_launch": dec_bytes},

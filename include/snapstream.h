@@ -11,7 +11,8 @@
  *                                  by zeroed padding rows when fewer exist.
  * The library fills that cache from a padded prefill (snap_compress), writes
  * each decoded token into its ring row (snap_cache_append, Sec. III-C), and
- * runs decode attention over the valid rows (snap_decode_attn).
+ * runs decode attention over the valid rows (snap_decode_attn; snap_decode_step
+ * does both for one layer).
  *
  * Conventions shared by every call
  *  - Token positions are 0-based; a prompt of length L holds tokens 0..L-1 and
@@ -171,6 +172,18 @@ snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, cons
                              const int32_t* n_topk, int32_t n, const int32_t* slot_ids,
                              const void* q, void* out, int32_t out_dtype, void* workspace,
                              size_t ws_bytes, void* stream);
+
+/* One layer's decode step (Sec. III-C): snap_cache_append(k_new, v_new)
+ * followed by snap_decode_attn, with the same arguments, results and cache
+ * contents as those two calls on the same stream.  For bf16 caches of the
+ * supported MFMA shapes both happen in one launch (the new token's row is read
+ * from k_new / v_new by the workgroup that attends it and stored into the
+ * cache in the same launch); other caches run the two launches.  The same
+ * workspace as snap_decode_attn; k_new / v_new must not alias the cache. */
+snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                             const int32_t* n_topk, int32_t n, const int32_t* slot_ids,
+                             const void* q, const void* k_new, const void* v_new, void* out,
+                             int32_t out_dtype, void* workspace, size_t ws_bytes, void* stream);
 
 /* pos[slot_ids[b]] += 1 for b < n (once per decode step, after every layer).
  * pos is device int32[n_slots]; slot ids outside [0, n_slots) are skipped. */

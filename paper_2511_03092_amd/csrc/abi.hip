@@ -169,7 +169,34 @@ snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, cons
   const size_t need = decode_geometry(*p, n).decode_bytes;
   if (!workspace || ((uintptr_t)workspace & 255u) || ws_bytes < need)
     return fail(SNAP_ERR_WORKSPACE, "workspace needs %zu bytes, 256-byte aligned (got %zu)", need, ws_bytes);
-  st = launch_decode(*p, *cache, pos, n_topk, n, slot_ids, q, out, out_dtype, workspace, (hipStream_t)stream);
+  st = launch_decode(*p, *cache, pos, n_topk, n, slot_ids, q, nullptr, nullptr, out, out_dtype, workspace,
+                     (hipStream_t)stream);
+  if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return st;
+}
+
+snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                             const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
+                             const void* k_new, const void* v_new, void* out, int32_t out_dtype, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  snap_status st = check_params(p);
+  if (st != SNAP_OK) return st;
+  if ((st = check_cache(p, cache)) != SNAP_OK) return st;
+  if (n < 0) return fail(SNAP_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return SNAP_OK;
+  if (!pos || !n_topk || !slot_ids) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids NULL");
+  if (!q || !aligned16(q)) return fail(SNAP_ERR_INVALID_ARG, "q is NULL or not 16-byte aligned");
+  if (!k_new || !aligned16(k_new)) return fail(SNAP_ERR_INVALID_ARG, "k_new is NULL or not 16-byte aligned");
+  if (!p->v_in_k && (!v_new || !aligned16(v_new)))
+    return fail(SNAP_ERR_INVALID_ARG, "v_new is NULL or not 16-byte aligned");
+  if (!out || !aligned16(out)) return fail(SNAP_ERR_INVALID_ARG, "out is NULL or not 16-byte aligned");
+  if (out_dtype != SNAP_F32 && out_dtype != SNAP_BF16) return fail(SNAP_ERR_INVALID_ARG, "out_dtype must be F32 or BF16");
+  const size_t need = decode_geometry(*p, n).decode_bytes;
+  if (!workspace || ((uintptr_t)workspace & 255u) || ws_bytes < need)
+    return fail(SNAP_ERR_WORKSPACE, "workspace needs %zu bytes, 256-byte aligned (got %zu)", need, ws_bytes);
+  st = launch_decode(*p, *cache, pos, n_topk, n, slot_ids, q, k_new, p->v_in_k ? nullptr : v_new, out, out_dtype,
+                     workspace, (hipStream_t)stream);
   if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
   return st;
 }

@@ -17,6 +17,12 @@
 namespace snap {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// Online softmax with a stale reference max: a head's reference moves only
+// when a block's max exceeds it by more than this (log2 units), so the
+// accumulators are rescaled on few blocks; probabilities stay <= 2^8.  Any
+// reference gives the same softmax (the combine merges chunks by their own
+// reference), only the rounding differs.
+constexpr float kStaleMax = 8.f;
 
 struct DecodeArgs {
   const void* q;         // [n][Hq][dk] (bf16 or fp32)
@@ -29,6 +35,10 @@ struct DecodeArgs {
   const int32_t* slot_ids;
   float* part;           // [n][Hq][n_chunks][dv]
   float2* ml;            // [n][Hq][n_chunks]  (max in log2 units, sum)
+  // fused append (bf16 caches only): the token at pos, [n][Hkv][dk] / [n][Hkv][dv];
+  // NULL when the launch only attends
+  const void* k_new;
+  const void* v_new;
   int Hq, Hkv, G, dk, dv, sink, recent, topk, n_slots, n_chunks, q_f32;
   float scale;
 };
@@ -41,12 +51,16 @@ struct RowSpan {
 // ring rows [0, n1), the rest the real top-K rows.
 __device__ __forceinline__ int virt_row(int v, int n1, int sr) { return v < n1 ? v : sr + (v - n1); }
 
+// Slot metadata is read with vector loads (the kernels also write global
+// memory, so the compiler cannot use the scalar cache); readfirstlane puts the
+// workgroup-uniform values back in scalar registers, which keeps the row loop
+// and its waits scalar control flow.
 __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, int& slot, RowSpan& sp) {
-  slot = a.slot_ids[b];
+  slot = __builtin_amdgcn_readfirstlane(a.slot_ids[b]);
   if (slot < 0 || slot >= a.n_slots) return false;
   const int sr = a.sink + a.recent;
-  const int p = a.pos[slot];
-  int nt = a.n_topk[slot];
+  const int p = __builtin_amdgcn_readfirstlane(a.pos[slot]);
+  int nt = __builtin_amdgcn_readfirstlane(a.n_topk[slot]);
   nt = nt < 0 ? 0 : (nt > a.topk ? a.topk : nt);
   const int n1 = p < 0 ? 0 : (p >= sr ? sr : p + 1);
   const int nv = n1 + nt;
@@ -56,6 +70,42 @@ __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, i
   sp.v0 = chunk * cs;
   sp.v1 = min(sp.v0 + cs, nv);
   return true;
+}
+
+// Fused append: the cache row of the token at pos[slot] (the ring update of
+// Sec. III-C; sinks are filled in place while pos < sink), or -1 when the
+// launch carries no new token.  The row lies in the first run of valid rows,
+// so its virtual index equals its cache row.  The workgroup that owns it reads
+// it from k_new/v_new, chunk 0 stores it into the cache, and nothing else in
+// the launch touches that row: no ordering between workgroups is needed.
+__device__ __forceinline__ int new_row(const DecodeArgs& a, int slot) {
+  if (!a.k_new) return -1;
+  const int p = __builtin_amdgcn_readfirstlane(a.pos[slot]);
+  if (p < 0) return -1;
+  return p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
+}
+
+// Chunk 0 of (slot, KV head g) stores the new k (and v) row, one 16-byte
+// piece per thread (dk/8 + dv/8 pieces, at most the workgroup size).  The
+// piece is fetched with the query and stored once that load has landed, so
+// the store adds no memory round trip of its own.
+__device__ __forceinline__ bool new_piece_load(const DecodeArgs& a, int b, int g, int i, u32x4& x) {
+  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
+  if (i >= kc + vc) return false;
+  if (i < kc)
+    x = *((const u32x4*)a.k_new + ((size_t)b * a.Hkv + g) * kc + i);
+  else
+    x = *((const u32x4*)a.v_new + ((size_t)b * a.Hkv + g) * vc + (i - kc));
+  return true;
+}
+__device__ __forceinline__ void new_piece_store(const DecodeArgs& a, int g, int slot, int row, int i, u32x4 x) {
+  const int B = a.sink + a.recent + a.topk;
+  const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + row;
+  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
+  if (i < kc)
+    *((u32x4*)const_cast<void*>(a.ck) + crow * kc + i) = x;
+  else
+    *((u32x4*)const_cast<void*>(a.cv) + crow * vc + (i - kc)) = x;
 }
 
 // ---------------------------------------------------------------- fp8 -> bf16
@@ -138,6 +188,11 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   const float xs = a.scale * kLog2e * ksc;
   const void* vbase = a.cv ? a.cv : a.ck;
   const int vstride = a.cv ? a.dv : a.dk;
+  // fused append (bf16 only): row vnew comes from k_new / v_new
+  const int vnew = FP8 ? -1 : new_row(a, slot);
+  const size_t knew_off = ((size_t)b * a.Hkv + g) * D, vnew_off = ((size_t)b * a.Hkv + g) * a.dv;
+  u32x4 newp = {0u, 0u, 0u, 0u};
+  const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, g, lane, newp);
 
   float m = -INFINITY, lsum = 0.f;
   f32x4 acc[VPASS][8];
@@ -149,12 +204,15 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   // K of block vb: lane's rows vb+l16 and vb+16+l16, k-slot group lg
   auto load_k = [&](int vb, RawT* ka, RawT* kb) {
     const int va = vb + l16, vb2 = vb + 16 + l16;
-    const size_t ra = row0 + virt_row(va, sp.n1, sr), rb = row0 + virt_row(vb2, sp.n1, sr);
+    const void* pa = va == vnew ? a.k_new : a.ck;
+    const void* pb = vb2 == vnew ? a.k_new : a.ck;
+    const size_t ea = va == vnew ? knew_off : (row0 + virt_row(va, sp.n1, sr)) * D;
+    const size_t eb = vb2 == vnew ? knew_off : (row0 + virt_row(vb2, sp.n1, sr)) * D;
 #pragma unroll
     for (int t = 0; t < KSTEPS; ++t) {
       const int col = 8 * (KSTEPS * lg + t);
-      ka[t] = load_raw8<FP8>(a.ck, ra * D + col, va < sp.v1);
-      kb[t] = load_raw8<FP8>(a.ck, rb * D + col, vb2 < sp.v1);
+      ka[t] = load_raw8<FP8>(pa, ea + col, va < sp.v1);
+      kb[t] = load_raw8<FP8>(pb, eb + col, vb2 < sp.v1);
     }
   };
   RawT ka[KSTEPS], kb[KSTEPS];
@@ -167,9 +225,10 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
-      const size_t rr = row0 + virt_row(vi, sp.n1, sr);
+      const void* pv = vi == vnew ? a.v_new : vbase;
+      const size_t ev = vi == vnew ? vnew_off : (row0 + virt_row(vi, sp.n1, sr)) * vstride;
 #pragma unroll
-      for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(vbase, rr * vstride + 128 * pp + 8 * l16, vi < sp.v1);
+      for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(pv, ev + 128 * pp + 8 * l16, vi < sp.v1);
     }
     RawT kn[KSTEPS], kn2[KSTEPS];
     if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
@@ -229,6 +288,7 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   }
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
+  if (has_newp) new_piece_store(a, g, slot, vnew, lane, newp);
   if (!hval) return;
   const size_t pi = ((size_t)b * a.Hq + qh) * a.n_chunks + chunk;
   if (lg == 0) a.ml[pi] = make_float2(m, lsum);
@@ -398,23 +458,29 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
 
 // ---------------------------------------------------------------- latent decode, LDS-staged
 // bf16 latent caches (576-wide rows, values = first 512 dims).  One workgroup
-// of 4 waves per (chunk, sequence) streams blocks of 32 rows through a
-// kLatStages-deep ring of LDS stages with direct global->LDS loads, so about
-// three blocks (110 KB) are in flight per CU while one is consumed.  Wave w
-// computes partial logits over its share of the 18 k-steps (5,5,4,4), the
-// four partials are summed through LDS in a fixed order, and wave w computes
-// the value product for dims [128w, 128w+128).
+// of 4 waves per (chunk, sequence) streams blocks of 32 rows through a ring
+// of LDS stages with direct global->LDS loads, so three blocks (110 KB) are in
+// flight per CU while one is consumed.  Wave w computes partial logits over
+// its share of the 18 k-steps (5,5,4,4), the four partials are summed through
+// LDS in a fixed order, and wave w computes the value product for dims
+// [128w, 128w+128).
 // LDS rows are 72 chunks of 16 bytes; chunk c of row r sits at slot
-// r*72 + (c ^ ((r >> 1) & 7)), which makes both the key-fragment reads (one
-// chunk of 16 consecutive rows) and the value reads (16 consecutive chunks of
-// one row) free of bank conflicts.
+// r*72 + (c ^ lat_swz(r)).  The row swizzle spreads the key-fragment reads
+// (one chunk of 16 consecutive rows) over the banks; the value reads
+// (consecutive chunks of one row) stay within aligned groups of 8 chunks.  Of
+// the swizzles measured with the LDS bank-conflict counter this one has the
+// fewest conflicts.
+// Four 36 KB stages (147 KB of the 160 KB LDS: one workgroup per CU); a
+// stage is refilled once every wave has consumed it, so four blocks are in
+// flight when block i is waited for.
 constexpr int kLatStages = 4;
 constexpr int kLatRowBytes = 576 * 2;
 constexpr int kLatChunks = kLatRowBytes / 16;        // 72
 constexpr int kLatBlockBytes = 32 * kLatRowBytes;    // 36864
 constexpr int kLatLoadsPerWave = 32 * kLatChunks / 64 / 4;  // 9 wave-instructions per block per wave
 
-__device__ __forceinline__ int lat_slot(int r, int c) { return r * kLatChunks + (c ^ ((r >> 1) & 7)); }
+__device__ __forceinline__ int lat_swz(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int lat_slot(int r, int c) { return r * kLatChunks + (c ^ lat_swz(r)); }
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr_t;
 // One wave-instruction of global -> LDS copy (lane i's 16 bytes land at
@@ -477,35 +543,54 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     }
   }
   // this lane's share of every block load: (row, chunk) of its 9 slots
-  int ld_r[kLatLoadsPerWave], ld_c[kLatLoadsPerWave];
+  int ld_r[kLatLoadsPerWave], ld_c[kLatLoadsPerWave], ld_off[kLatLoadsPerWave];
 #pragma unroll
   for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
     const int q = (wu + 4 * ii) * 64 + lane;
     const int r = q / kLatChunks, cs = q % kLatChunks;
     ld_r[ii] = r;
-    ld_c[ii] = cs ^ ((r >> 1) & 7);
+    ld_c[ii] = cs ^ lat_swz(r);
+    ld_off[ii] = r * kLatRowBytes + ld_c[ii] * 16;
   }
   const unsigned char* cache = (const unsigned char*)a.ck + (size_t)slot * B * kLatRowBytes;
-  const int nblk = (sp.v1 - sp.v0 + 31) / 32;
+  // fused append: row vnew comes from k_new
+  const int vnew = new_row(a, slot);
+  const unsigned char* knew = vnew >= 0 ? (const unsigned char*)a.k_new + (size_t)b * kLatRowBytes : nullptr;
+  u32x4 newp = {0u, 0u, 0u, 0u};
+  const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, 0, threadIdx.x, newp);
+  const int nblk = __builtin_amdgcn_readfirstlane((sp.v1 - sp.v0 + 31) / 32);
   auto issue = [&](int blk) {
     const int vb = sp.v0 + 32 * blk;
     unsigned char* dst = &stage[blk % kLatStages][0];
+    // a whole block inside one run of the row map, without the new token:
+    // 32 consecutive cache rows from a uniform base
+    const bool plain = vb + 32 <= sp.v1 && (vb + 32 <= sp.n1 || vb >= sp.n1) && !(vnew >= vb && vnew < vb + 32);
+    if (plain) {
+      const unsigned char* base = cache + (size_t)virt_row(vb, sp.n1, sr) * kLatRowBytes;
 #pragma unroll
-    for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
-      int v = vb + ld_r[ii];
-      v = v < sp.v1 ? v : sp.v1 - 1;
-      const unsigned char* src = cache + (size_t)virt_row(v, sp.n1, sr) * kLatRowBytes + ld_c[ii] * 16;
-      dma16_lat(src, dst + (size_t)(wu + 4 * ii) * 1024);
+      for (int ii = 0; ii < kLatLoadsPerWave; ++ii) dma16_lat(base + ld_off[ii], dst + (size_t)(wu + 4 * ii) * 1024);
+    } else {
+#pragma unroll
+      for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
+        int v = vb + ld_r[ii];
+        v = v < sp.v1 ? v : sp.v1 - 1;
+        const unsigned char* src =
+            (v == vnew ? knew : cache + (size_t)virt_row(v, sp.n1, sr) * kLatRowBytes) + ld_c[ii] * 16;
+        dma16_lat(src, dst + (size_t)(wu + 4 * ii) * 1024);
+      }
     }
   };
 
   const float xs = a.scale * kLog2e;
-  float m = -INFINITY, lsum = 0.f;
+  float m = -INFINITY, mref = 0.f, lsum = 0.f;  // reference max (log2 units), its finite stand-in, sum
   f32x4 acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  lat_wait_vm<0>();  // query fragments landed; from here vmcnt counts block loads only
+  lat_wait_vm<0>();  // query fragments (and the new row's piece) landed
+  // The store is counted by vmcnt with the block loads issued after it; loads
+  // complete in order, so the waits below still cover the blocks they name.
+  if (has_newp) new_piece_store(a, 0, slot, vnew, threadIdx.x, newp);
   for (int s = 0; s < kLatStages && s < nblk; ++s) issue(s);
 
   for (int i = 0; i < nblk; ++i) {
@@ -539,30 +624,43 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     lat_barrier();
     s0 = ((sx[0][0][lane] + sx[1][0][lane]) + sx[2][0][lane]) + sx[3][0][lane];
     s1 = ((sx[0][1][lane] + sx[1][1][lane]) + sx[2][1][lane]) + sx[3][1][lane];
+    // raw dot products; the scale (> 0) is applied to the block max and folded
+    // into the exponent
     float x[8];
+    if (vb + 32 <= sp.v1) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
-      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        x[e] = s0[e];
+        x[4 + e] = s1[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] : -INFINITY;
+        x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] : -INFINITY;
+      }
     }
     float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
     bm = fmaxf(bm, __shfl_xor(bm, 16));
     bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float mn = fmaxf(m, bm);
-    float alpha = 1.f, pe[8];
-    if (mn == -INFINITY) {
+    bm *= xs;
+    const bool up = bm > m + kStaleMax;  // always true for the first valid block (m = -inf)
+    if (wave_any(up)) {
+      const float mnew = up ? bm : m;
+      const float alpha = up ? fast_exp2(m - mnew) : 1.f;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) pe[k] = 0.f;
-    } else {
-      alpha = fast_exp2(m - mn);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) pe[k] = fast_exp2(x[k] - mn);
+      for (int c = 0; c < 8; ++c) acc[c] *= alpha;
+      lsum *= alpha;
+      m = mnew;
+      mref = m == -INFINITY ? 0.f : m;  // no valid row yet: every x is -inf, exp2 gives 0
     }
-    m = mn;
-    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    float pe[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pe[k] = fast_exp2(fmaf(x[k], xs, -mref));
+    lsum += ((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7]));
     u32x4 pw;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) pw[k] = f32_to_bf16_bits(pe[2 * k]) | (f32_to_bf16_bits(pe[2 * k + 1]) << 16);
+    for (int k = 0; k < 4; ++k) pw[k] = pack_bf16x2(pe[2 * k], pe[2 * k + 1]);
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
     u32x4 vv[8];
 #pragma unroll
@@ -577,7 +675,6 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
       u32x4 av;
 #pragma unroll
       for (int k = 0; k < 4; ++k) av[k] = __builtin_amdgcn_perm(vv[2 * k + 1][u], vv[2 * k][u], selb);
-      acc[c] *= alpha;
       acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[c], 0, 0, 0);
     }
     lat_barrier();  // every wave is done with this stage
@@ -814,6 +911,11 @@ __global__ __launch_bounds__(256) void advance(int32_t* pos, int n_slots, int n,
 // ---------------------------------------------------------------- host side
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// workgroups per call for the LDS-staged latent decode: one per CU, all
+// resident at once (more, smaller chunks measured slower: each workgroup pays
+// its prologue and the combine grows)
+constexpr int kLatentLdsWGs = 256;
+
 Geometry decode_geometry(const snap_params& p, int n) {
   Geometry g{};
   const int B = p.sink + p.recent + p.topk;
@@ -821,7 +923,7 @@ Geometry decode_geometry(const snap_params& p, int n) {
   // latent caches run 4-wave workgroups (two per CU), the others one wave each
   const bool latent = p.v_in_k && p.d_qk == 576;
   const bool latent_lds = latent && p.kv_dtype == SNAP_BF16;  // one 4-wave workgroup per CU (LDS-bound)
-  const int target = latent_lds ? 256 : (latent ? 512 : 2048);
+  const int target = latent_lds ? kLatentLdsWGs : (latent ? 512 : 2048);
   const int min_rows = latent ? 256 : 128;
   int want = (target + units - 1) / units;
   int maxc = (B + min_rows - 1) / min_rows;
@@ -838,8 +940,8 @@ Geometry decode_geometry(const snap_params& p, int n) {
 }
 
 snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32_t* pos, const int32_t* n_topk,
-                          int n, const int32_t* slot_ids, const void* q, void* out, int out_dtype, void* ws,
-                          hipStream_t stream) {
+                          int n, const int32_t* slot_ids, const void* q, const void* k_new, const void* v_new,
+                          void* out, int out_dtype, void* ws, hipStream_t stream) {
   Geometry geo = decode_geometry(p, n);
   DecodeArgs a;
   a.q = q;
@@ -864,11 +966,24 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
   a.n_chunks = geo.n_chunks;
   a.q_f32 = p.in_dtype == SNAP_F32;
   a.scale = p.sm_scale > 0.f ? p.sm_scale : 1.0f / sqrtf((float)p.d_qk);
+  a.k_new = nullptr;
+  a.v_new = nullptr;
 
   const bool mfma_ok = p.in_dtype == SNAP_BF16 && !p.v_in_k && p.d_qk == 128 && p.d_v == 128 &&
                        (p.kv_dtype == SNAP_BF16 || p.kv_dtype == SNAP_FP8_E4M3);
   const bool mla_ok = p.in_dtype == SNAP_BF16 && p.v_in_k && p.n_kv_heads == 1 && p.d_qk == 576 && p.d_v == 512 &&
                       (p.kv_dtype == SNAP_BF16 || p.kv_dtype == SNAP_FP8_E4M3);
+  if (k_new) {
+    // the bf16 MFMA kernels take the new token in the same launch; the others
+    // run the append kernel first (same result)
+    if ((mla_ok || mfma_ok) && p.kv_dtype == SNAP_BF16) {
+      a.k_new = k_new;
+      a.v_new = p.v_in_k ? nullptr : v_new;
+    } else {
+      const snap_status st = launch_append(p, c, pos, n, slot_ids, k_new, v_new, stream);
+      if (st != SNAP_OK) return st;
+    }
+  }
   if (mla_ok) {
     dim3 grid(geo.n_chunks, n);
     if (p.kv_dtype == SNAP_FP8_E4M3)

@@ -18,6 +18,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------- numerics
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
@@ -29,6 +31,16 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   u += 0x7fffu + ((u >> 16) & 1u);
   return u >> 16;
 }
+
+// Two fp32 -> packed bf16 pair (lo in the low half), round to nearest even:
+// one v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// true when pred holds in any lane of the wave (wave-uniform)
+__device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
 
 // fp32 -> OCP E4M3 code: round to nearest even, saturate at +-448, NaN -> 0x7F.
 __device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
@@ -108,9 +120,12 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
 snap_status launch_append(const snap_params& p, const snap_cache& c, const int32_t* pos, int n,
                           const int32_t* slot_ids, const void* k_new, const void* v_new,
                           hipStream_t stream);
+// k_new / v_new non-NULL: append the token at pos first (fused into the
+// attention launch for bf16 caches), as snap_cache_append would
 snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32_t* pos,
                           const int32_t* n_topk, int n, const int32_t* slot_ids, const void* q,
-                          void* out, int out_dtype, void* ws, hipStream_t stream);
+                          const void* k_new, const void* v_new, void* out, int out_dtype, void* ws,
+                          hipStream_t stream);
 snap_status launch_advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids, hipStream_t stream);
 
 void set_error(const char* fmt, ...);

@@ -170,9 +170,10 @@ def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gse
 
 
 def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, steps, out_dtype, tol,
-                 check_every=1, layer=0, salt=0):
+                 check_every=1, layer=0, salt=0, fused=False):
     """Run `steps` decode steps (append, attend, advance) and check each checked
-    step against the oracle on the GPU's cache.  Returns the max abs error."""
+    step against the oracle on the GPU's cache.  Returns the max abs error.
+    fused: append and attend through snap_decode_step instead of two calls."""
     dev = cache.k.device
     sl = torch.tensor(slots, dtype=torch.int32, device=dev)
     n = len(slots)
@@ -186,8 +187,12 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
         check = (step % check_every == 0) or step == steps - 1
         if check:
             before_k, before_v = cache.host_values()
-        snap.snap_cache_append(p, cache.c(), cache.pos, sl, kn.to(dev), None if vn is None else vn.to(dev))
-        snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), out, ws)
+        if fused:
+            snap.snap_decode_step(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), kn.to(dev),
+                                  None if vn is None else vn.to(dev), out, ws)
+        else:
+            snap.snap_cache_append(p, cache.c(), cache.pos, sl, kn.to(dev), None if vn is None else vn.to(dev))
+            snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), out, ws)
         snap.snap_advance(cache.pos, sl)
         torch.cuda.synchronize()
         if not check:
