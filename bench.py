@@ -52,7 +52,6 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--event-every", type=int, default=16, help="time decode calls of every n-th decode step")
     ap.add_argument("--two-calls", action="store_true",
                     help="decode with snap_cache_append + snap_decode_attn instead of snap_decode_step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -120,25 +119,25 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # ---- one step
+    # ---- one step.  Events bracket whole phases (every layer's compress; the
+    # whole decode loop), never single calls: an event record costs device
+    # time of its own, which would be charged to the call it brackets.
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
     def step(timing):
+        if timing is not None:
+            c0 = ev()
         for l in range(layers):
             q, k, v = prompts[l]
-            if timing is not None:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
             snap.snap_compress(p, caches[l][2], pos, ntop, slots, lens, q, k, v, wsc, stream=sptr)
-            if timing is not None:
-                e1 = torch.cuda.Event(enable_timing=True)
-                e1.record(stream)
-                timing["compress"].append((e0, e1))
+        if timing is not None:
+            timing["compress"].append((c0, ev()))
         for t in range(dsteps):
-            sample = timing is not None and (t % args.event_every == 0)
             for l in range(layers):
                 qd, kd, vd = dec[l]
-                if sample:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
                 if args.two_calls:
                     snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t],
                                            stream=sptr)
@@ -146,11 +145,9 @@ def main():
                 else:
                     snap.snap_decode_step(p, caches[l][2], pos, ntop, slots, qd[t], kd[t],
                                           None if vd is None else vd[t], out, wsd, stream=sptr)
-                if sample:
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e1.record(stream)
-                    timing["decode"].append((e0, e1))
             snap.snap_advance(pos, slots, stream=sptr)
+        if timing is not None:
+            timing["decode"].append((timing["compress"][-1][1], ev()))
 
     for _ in range(args.warmup):
         step(None)
@@ -166,8 +163,11 @@ def main():
     torch.cuda.synchronize()
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
-    comp_ms = sum(a.elapsed_time(b) for a, b in timing["compress"]) / max(len(timing["compress"]), 1)
-    dec_ms = sum(a.elapsed_time(b) for a, b in timing["decode"]) / max(len(timing["decode"]), 1)
+    # per layer call: phase time / calls (the decode phase includes one
+    # snap_advance per step, shared by that step's layer calls)
+    comp_ms = sum(a.elapsed_time(b) for a, b in timing["compress"]) / (args.steps * layers)
+    dec_ms = (sum(a.elapsed_time(b) for a, b in timing["decode"]) / (args.steps * dsteps * layers)
+              if dsteps else 0.0)
 
     # ---- algorithmic bytes of one layer's decode step: valid rows + q + out, plus
     # the appended token (read from the input, written to its cache row)
@@ -185,6 +185,15 @@ def main():
     new_bytes = n * wl.n_kv_heads * (wl.d_qk + (0 if wl.v_in_k else wl.d_v)) * in_elt + n * wl.n_kv_heads * row_bytes
     dec_bytes = valid * wl.n_kv_heads * row_bytes + q_bytes + o_bytes + new_bytes
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9 if dec_ms > 0 else 0.0
+    # ---- score GEMM (Q_obs x K^T of both compress passes) against the bf16 MFMA
+    # peak: useful flops over the whole compress call, a lower bound on the
+    # score kernels' own utilisation (the call also pools, selects and gathers)
+    G = wl.n_q_heads // wl.n_kv_heads
+    score_flop = 0
+    for L in lengths:
+        keys = max(L - s_r, 0)  # candidates: the normaliser domain of both passes
+        score_flop += wl.n_kv_heads * 2 * G * min(wl.obs_window, L) * wl.d_qk * keys
+    score_tflops = 2 * score_flop / (comp_ms * 1e-3) / 1e12 if comp_ms > 0 else 0.0
     tokens = n * dsteps
     value = tokens / (ms_step * 1e-3)
     decode_ms_per_token_step = dec_ms * layers  # attention only, per decode step (all layers)
@@ -212,6 +221,9 @@ def main():
         "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1) if dec_ms > 0 else 0.0,
         "compress_ms_per_layer_call": round(comp_ms, 4),
         "compress_ms_per_seq_layer": round(comp_ms / n, 4),
+        "score_gemm": {"gflop_per_layer_call_one_pass": round(score_flop / 1e9, 2), "passes": 2,
+                       "tflops_over_compress_call": round(score_tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
+                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4)},
         "roofline": {"bound": "hbm",
                      "kernel": ("snap_cache_append + snap_decode_attn" if args.two_calls else
                                 "snap_decode_step (append + split-K attention, one launch) + combine"),
@@ -225,13 +237,14 @@ def main():
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value):
+def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value, comp_budget_s=10.0, dec_budget_s=2.0):
     """The fp64 oracle, single-threaded on the host, on a bounded sample of the
-    same workload: one compress unit (one sequence x one KV head) at the
-    longest prompt and a few decode units (one sequence x one KV head x one
-    step), extrapolated to a whole step by unit counts."""
+    same workload: compress units (one sequence x one KV head) at the longest
+    prompt, cycling over the KV heads, until about comp_budget_s of work, and
+    decode units (one sequence x one KV head x one step) over the cache that
+    built, until about dec_budget_s; extrapolated to a whole step by unit
+    counts (compress scaled by each sequence's length)."""
     import numpy as np
-    import torch
 
     import oracle
     import synth
@@ -241,25 +254,33 @@ def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value):
     L = max(lengths)
     q, k, v = synth.prefill(wl, 0, 0, L, device="cpu")
     G = op.group
-    t = time.time()
-    res = oracle.compress_group(op, L, oracle.f64(q[:G]), oracle.f64(k[0]), None if v is None else oracle.f64(v[0]))
-    t_comp = time.time() - t
-    # decode units over the just-built cache
+    n_comp, t_all, res = 0, 0.0, None
+    while t_all < comp_budget_s and n_comp < 64:
+        g = n_comp % p.n_kv_heads
+        qg, kg = oracle.f64(q[g * G:(g + 1) * G]), oracle.f64(k[g])
+        vg = None if v is None else oracle.f64(v[g])
+        t = time.time()
+        r_ = oracle.compress_group(op, L, qg, kg, vg)
+        t_all += time.time() - t
+        res = res or r_
+        n_comp += 1
+    t_comp = t_all / n_comp
     qd = np.random.default_rng(0).normal(size=(G, p.d_qk))
-    reps = 4
-    t = time.time()
-    for _ in range(reps):
+    n_dec, t_all = 0, 0.0
+    while t_all < dec_budget_s and n_dec < 4096:
+        t = time.time()
         oracle.decode_attn_group(op, L, len(res.sel), qd, res.cache_k, res.cache_v)
-    t_dec = (time.time() - t) / reps
-    units_comp = layers * n * p.n_kv_heads  # (scaled by each sequence's length)
+        t_all += time.time() - t
+        n_dec += 1
+    t_dec = t_all / n_dec
+    units_comp = layers * n * p.n_kv_heads
     comp_s = sum(t_comp * (Lb / L) for Lb in lengths) * layers * p.n_kv_heads
     dec_s = t_dec * layers * n * p.n_kv_heads * dsteps
-    step_s = comp_s + dec_s
-    val = n * dsteps / step_s
+    val = n * dsteps / (comp_s + dec_s)
     return {"value": float(f"{val:.6g}"), "unit": "tok/s", "cores": 1, "kind": "oracle",
-            "sample": (f"1 compress unit (1 sequence x 1 KV head, L={L}) in {t_comp:.2f}s and {reps} decode units "
-                       f"(1 sequence x 1 KV head x 1 step) at {t_dec * 1e3:.1f} ms each, single thread; extrapolated "
-                       f"to {units_comp} compress units (scaled by length) and "
+            "sample": (f"{n_comp} compress units (1 sequence x 1 KV head, L={L}) at {t_comp:.2f} s each and "
+                       f"{n_dec} decode units (1 sequence x 1 KV head x 1 step) at {t_dec * 1e3:.1f} ms each, "
+                       f"single thread; extrapolated to {units_comp} compress units (scaled by length) and "
                        f"{layers * n * p.n_kv_heads * dsteps} decode units per step"),
             "gpu_over_cpu": float(f"{gpu_value / val:.4g}")}
 

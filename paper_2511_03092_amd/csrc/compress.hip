@@ -226,9 +226,9 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
       }
   } else {
     lds_barrier();
-    if (threadIdx.x < kKeyTile) {
-      int j = t0 + threadIdx.x;
-      const float* c = colbuf + threadIdx.x;
+    if (tid() < kKeyTile) {
+      int j = t0 + tid();
+      const float* c = colbuf + tid();
       float sum;
       if constexpr (NW == 4) {
         sum = (c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile]);
@@ -259,10 +259,10 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
   __shared__ float colbuf[NW * kKeyTile];
   __shared__ float qlds[kBF16 ? 1 : 128 * D];           // fp32 inputs: [rows_pad <= 128][D]
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = tid() & 63, wave = tid() >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
-  const int bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
-  int L = a.lengths[b];
+  const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
+  int L = uniform(a.lengths[b]);
   L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
   const int s = a.sink, r = a.recent;
   const int clo = s, chi = L - r;  // candidates [clo, chi)
@@ -274,7 +274,7 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
     lo = 0;
     hi = L;
   }
-  const int c0 = lo + blockIdx.x * a.key_chunk;
+  const int c0 = lo + bid_x() * a.key_chunk;
   const int c1 = min(c0 + a.key_chunk, hi);
   const int we = min(a.w, L);
   const bool wave_has_rows = wave * 32 < a.rows;
@@ -290,10 +290,10 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
       sl.rpos[rb][e] = L - a.w + ii;
     }
 
-  float2* st_out = a.stats + ((size_t)bg * a.n_kchunks + blockIdx.x) * a.rows_pad;
+  float2* st_out = a.stats + ((size_t)bg * a.n_kchunks + bid_x()) * a.rows_pad;
   if (c0 >= c1) {
     if (!COLSUM) {
-      for (int t = threadIdx.x; t < a.rows_pad; t += blockDim.x) st_out[t] = make_float2(-INFINITY, 0.f);
+      for (int t = tid(); t < a.rows_pad; t += nthreads()) st_out[t] = make_float2(-INFINITY, 0.f);
     }
     return;
   }
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
       }
     }
   } else {
-    for (int i = threadIdx.x; i < a.rows_pad * D; i += blockDim.x) {
+    for (int i = tid(); i < a.rows_pad * D; i += nthreads()) {
       int rho = i / D;
       qlds[i] = rho < a.rows ? ((const float*)qbase)[i] : 0.f;
     }
@@ -419,9 +419,9 @@ struct ReduceArgs {
 // of each group also resets the group's selection scratch.
 constexpr int kReduceLanes = 8;
 __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
-  const int bg = blockIdx.y, b = bg / a.Hkv;
-  const int sub = threadIdx.x % kReduceLanes;
-  const int rho = blockIdx.x * (256 / kReduceLanes) + threadIdx.x / kReduceLanes;
+  const int bg = bid_y(), b = bg / a.Hkv;
+  const int sub = tid() % kReduceLanes;
+  const int rho = bid_x() * (256 / kReduceLanes) + tid() / kReduceLanes;
   const float2* st = a.stats + (size_t)bg * a.n_kchunks * a.rows_pad;
   if (rho < a.rows_pad) {
     float m = -INFINITY;
@@ -452,13 +452,13 @@ __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
       a.rowref[(size_t)bg * a.rows_pad + rho] = ref;
     }
   }
-  if (blockIdx.x != 0) return;
+  if (bid_x() != 0) return;
   for (int pass = 0; pass < 3; ++pass) {
     uint32_t* h = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
-    for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) h[i] = 0u;
+    for (int i = tid(); i < kRadixBins; i += nthreads()) h[i] = 0u;
   }
-  if (threadIdx.x == 0) {
-    int L = a.lengths[b];
+  if (tid() == 0) {
+    int L = uniform(a.lengths[b]);
     L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
     int n = L - a.sink - a.recent;
     n = n < 0 ? 0 : n;
@@ -487,9 +487,20 @@ struct SelectArgs {
   int groups, Hkv, max_len, sink, recent, topk, pool_kernel, pool, n_splits;
 };
 
+// the group's selection state, with every field in scalar registers
+__device__ __forceinline__ RadixState load_state(const RadixState* p) {
+  RadixState s = *p;
+  s.prefix = (uint32_t)uniform((int)s.prefix);
+  s.mask = (uint32_t)uniform((int)s.mask);
+  s.krem = uniform(s.krem);
+  s.keff = uniform(s.keff);
+  s.mode = uniform(s.mode);
+  return s;
+}
+
 __device__ __forceinline__ void seq_range(const SelectArgs& a, int bg, int& c0, int& c1) {
   int b = bg / a.Hkv;
-  int L = a.lengths[b];
+  int L = uniform(a.lengths[b]);
   L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
   c0 = a.sink;
   c1 = L - a.recent;
@@ -512,7 +523,7 @@ __device__ __forceinline__ void radix_flush(const SelectArgs& a, int bg, int pas
   const int nb = pass == 2 ? 1024 : 2048;
   uint32_t* gh = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
   __syncthreads();
-  for (int i = threadIdx.x; i < nb; i += blockDim.x) {
+  for (int i = tid(); i < nb; i += nthreads()) {
     uint32_t v = 0;
 #pragma unroll
     for (int w = 0; w < kSubHists; ++w) v += lhist[w][i];
@@ -521,7 +532,7 @@ __device__ __forceinline__ void radix_flush(const SelectArgs& a, int bg, int pas
 }
 
 __device__ __forceinline__ void clear_hists(uint32_t (*lhist)[kRadixBins]) {
-  for (int i = threadIdx.x; i < kSubHists * kRadixBins; i += blockDim.x) (&lhist[0][0])[i] = 0u;
+  for (int i = tid(); i < kSubHists * kRadixBins; i += nthreads()) (&lhist[0][0])[i] = 0u;
 }
 
 // P = pool(A) on this workgroup's candidates (+ the debug copy) and the first
@@ -529,30 +540,30 @@ __device__ __forceinline__ void clear_hists(uint32_t (*lhist)[kRadixBins]) {
 __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
   __shared__ float la[kCandChunk + 64];
   __shared__ uint32_t lhist[kSubHists][kRadixBins];
-  const int bg = blockIdx.y, split = blockIdx.x;
-  const int wave = threadIdx.x >> 6;
+  const int bg = bid_y(), split = bid_x();
+  const int wave = tid() >> 6;
   int c0, c1;
   seq_range(a, bg, c0, c1);
   const int half = a.pool_kernel / 2;
   const int j0 = c0 + split * kCandChunk, j1 = min(j0 + kCandChunk, c1);
-  const RadixState st = a.state[bg];
+  const RadixState st = load_state(&a.state[bg]);
   float* Pg = a.P + (size_t)bg * a.max_len;
 
   if (a.pooled_out && split == 0) {
     float* po = a.pooled_out + (size_t)bg * a.max_len;
-    for (int j = threadIdx.x; j < a.max_len; j += blockDim.x)
+    for (int j = tid(); j < a.max_len; j += nthreads())
       if (j < c0 || j >= c1) po[j] = __uint_as_float(kQuietNaN);
   }
   if (st.mode == 2) clear_hists(lhist);
   if (j0 < j1) {
     const float* Ag = a.A + (size_t)bg * a.max_len;
     const float padv = a.pool == SNAP_POOL_MAX ? -INFINITY : 0.f;
-    for (int i = threadIdx.x; i < (j1 - j0) + 2 * half; i += blockDim.x) {
+    for (int i = tid(); i < (j1 - j0) + 2 * half; i += nthreads()) {
       int t = j0 - half + i;
       la[i] = (t >= c0 && t < c1) ? Ag[t] : padv;
     }
     __syncthreads();
-    for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+    for (int j = j0 + tid(); j < j1; j += nthreads()) {
       const float* w = la + (j - j0);
       float v;
       if (a.pool == SNAP_POOL_MAX) {
@@ -573,9 +584,9 @@ __global__ __launch_bounds__(kSelThreads) void pool_hist0(SelectArgs a) {
 
 __global__ __launch_bounds__(kSelThreads) void radix_pass(SelectArgs a, int pass) {
   __shared__ uint32_t lhist[kSubHists][kRadixBins];
-  const int bg = blockIdx.y, split = blockIdx.x;
-  const int wave = threadIdx.x >> 6;
-  const RadixState st = a.state[bg];
+  const int bg = bid_y(), split = bid_x();
+  const int wave = tid() >> 6;
+  const RadixState st = load_state(&a.state[bg]);
   if (st.mode != 2) return;
   int c0, c1;
   seq_range(a, bg, c0, c1);
@@ -583,7 +594,7 @@ __global__ __launch_bounds__(kSelThreads) void radix_pass(SelectArgs a, int pass
   clear_hists(lhist);
   __syncthreads();
   const float* Pg = a.P + (size_t)bg * a.max_len;
-  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+  for (int j = j0 + tid(); j < j1; j += nthreads()) {
     uint32_t bits = __float_as_uint(Pg[j]);
     if ((bits & st.mask) == st.prefix) atomicAdd(&lhist[wave][radix_digit(bits, pass)], 1u);
   }
@@ -597,13 +608,13 @@ __global__ __launch_bounds__(kSelThreads) void radix_pass(SelectArgs a, int pass
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total);
 __global__ __launch_bounds__(kSelThreads) void radix_scan(SelectArgs a, int pass) {
   __shared__ uint32_t lds[8];
-  const int bg = blockIdx.x;
-  RadixState st = a.state[bg];
+  const int bg = bid_x();
+  RadixState st = load_state(&a.state[bg]);
   if (st.mode != 2) return;
   const int nb = pass == 2 ? 1024 : 2048;
   const int per = nb / kSelThreads;  // 8 or 4
   const uint32_t* gh = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
-  const int top = nb - per * threadIdx.x;  // this thread's bins: [top - per, top)
+  const int top = nb - per * tid();  // this thread's bins: [top - per, top)
   uint32_t hv[8];
   uint32_t tot = 0;
   for (int i = 0; i < per; ++i) {
@@ -631,7 +642,7 @@ __global__ __launch_bounds__(kSelThreads) void radix_scan(SelectArgs a, int pass
 
 // block-wide exclusive scan of one value per thread (kSelThreads threads)
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = tid() & 63, wave = tid() >> 6;
   uint32_t x = v;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -655,15 +666,15 @@ constexpr int kPerThread = kCandChunk / kSelThreads;  // 8 consecutive candidate
 
 __global__ __launch_bounds__(kSelThreads) void select_count(SelectArgs a) {
   __shared__ uint32_t lds[8];
-  const int bg = blockIdx.y, split = blockIdx.x;
-  const RadixState st = a.state[bg];
+  const int bg = bid_y(), split = bid_x();
+  const RadixState st = load_state(&a.state[bg]);
   if (st.mode != 2) return;
   int c0, c1;
   seq_range(a, bg, c0, c1);
   const int j0 = c0 + split * kCandChunk, j1 = min(j0 + kCandChunk, c1);
   const float* Pg = a.P + (size_t)bg * a.max_len;
   uint32_t gt = 0, eq = 0;
-  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+  for (int j = j0 + tid(); j < j1; j += nthreads()) {
     uint32_t bits = __float_as_uint(Pg[j]);
     gt += bits > st.prefix;
     eq += bits == st.prefix;
@@ -671,22 +682,22 @@ __global__ __launch_bounds__(kSelThreads) void select_count(SelectArgs a) {
   uint32_t tg, te;
   block_exclusive_scan(gt, lds, tg);
   block_exclusive_scan(eq, lds, te);
-  if (threadIdx.x == 0) a.counts[(size_t)bg * a.n_splits + split] = make_uint2(tg, te);
+  if (tid() == 0) a.counts[(size_t)bg * a.n_splits + split] = make_uint2(tg, te);
 }
 
 // Ordered compaction: a candidate is kept when P > t, or P == t and it is among
 // the krem lowest-index candidates equal to t.  Output is in token order.
 __global__ __launch_bounds__(kSelThreads) void select_write(SelectArgs a) {
   __shared__ uint32_t lds[8];
-  const int bg = blockIdx.y, split = blockIdx.x;
-  const RadixState st = a.state[bg];
+  const int bg = bid_y(), split = bid_x();
+  const RadixState st = load_state(&a.state[bg]);
   if (st.mode == 0) return;
   int c0, c1;
   seq_range(a, bg, c0, c1);
   const int j0 = c0 + split * kCandChunk, j1 = min(j0 + kCandChunk, c1);
   int32_t* sg = a.sel + (size_t)bg * a.topk;
   if (st.mode == 1) {
-    for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) sg[j - c0] = j;
+    for (int j = j0 + tid(); j < j1; j += nthreads()) sg[j - c0] = j;
     return;
   }
   uint32_t gt_before = 0, eq_before = 0;
@@ -699,7 +710,7 @@ __global__ __launch_bounds__(kSelThreads) void select_write(SelectArgs a) {
   const uint32_t ties_here = krem > eq_before ? krem - eq_before : 0u;
   const uint32_t out_base = gt_before + (eq_before < krem ? eq_before : krem);
   const float* Pg = a.P + (size_t)bg * a.max_len;
-  const int jt = j0 + threadIdx.x * kPerThread;
+  const int jt = j0 + tid() * kPerThread;
   uint32_t bits[kPerThread];
   uint32_t neq = 0;
 #pragma unroll
@@ -807,24 +818,24 @@ __device__ __forceinline__ void copy8(const In* src, Out* dst, float scale) {
 // head); threads walk (row, 8-element piece) pairs so every lane copies.
 template <typename In, typename Out>
 __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
-  const int bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
-  const int slot = a.slot_ids[b];
+  const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
+  const int slot = uniform(a.slot_ids[b]);
   const int s = a.sink, r = a.recent, B = s + r + a.topk;
-  int L = a.lengths[b];
+  int L = uniform(a.lengths[b]);
   L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
-  const int keff = a.state[bg].keff;
+  const int keff = uniform(a.state[bg].keff);
   const int32_t* sg = a.sel + (size_t)bg * a.topk;
-  const int row0 = blockIdx.x * a.rows_per_block;
+  const int row0 = bid_x() * a.rows_per_block;
   const int row1 = min(row0 + a.rows_per_block, B);
 
   if (a.sel_out) {
-    for (int m = row0 + threadIdx.x; m < row1; m += blockDim.x) {
+    for (int m = row0 + tid(); m < row1; m += nthreads()) {
       int mm = m - s - r;
       if (mm >= 0) a.sel_out[(size_t)bg * a.topk + mm] = mm < keff ? sg[mm] : -1;
     }
   }
   if (slot < 0 || slot >= a.n_slots) return;
-  if (blockIdx.x == 0 && g == 0 && threadIdx.x == 0) {
+  if (bid_x() == 0 && g == 0 && tid() == 0) {
     a.pos[slot] = L;
     a.n_topk[slot] = keff;
   }
@@ -834,7 +845,7 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const float vs = (sizeof(Out) == 1 && a.v) ? a.v_scale[(size_t)slot * a.Hkv + g] : 1.f;
   const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
   const int items = (row1 - row0) * per_row;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+  for (int it = tid(); it < items; it += nthreads()) {
     const int row = row0 + it / per_row, piece = it % per_row;
     const int t = row_source(row, L, s, r, keff, sg);
     if (piece < kp) {

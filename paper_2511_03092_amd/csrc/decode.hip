@@ -161,8 +161,8 @@ template <int KSTEPS, int VPASS, bool FP8>
 __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   constexpr int D = KSTEPS * 32;
   typedef typename Raw8<FP8>::T RawT;
-  const int lane = threadIdx.x, l16 = lane & 15, lg = lane >> 4;
-  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / a.Hkv, g = bg % a.Hkv;
+  const int lane = tid(), l16 = lane & 15, lg = lane >> 4;
+  const int chunk = bid_x(), bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
   int slot;
   RowSpan sp;
   if (!span_of(a, b, chunk, slot, sp)) return;
@@ -194,15 +194,30 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   u32x4 newp = {0u, 0u, 0u, 0u};
   const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, g, lane, newp);
 
-  float m = -INFINITY, lsum = 0.f;
+  float m = -INFINITY, mref = 0.f, lsum = 0.f;  // reference max (log2 units), its finite stand-in, sum
   f32x4 acc[VPASS][8];
 #pragma unroll
   for (int pp = 0; pp < VPASS; ++pp)
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[pp][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // a whole block inside one run of the row map, without the new token: 32
+  // consecutive cache rows from a uniform base (wave-uniform test)
+  auto plain = [&](int vb) {
+    return vb + 32 <= sp.v1 && (vb + 32 <= sp.n1 || vb >= sp.n1) && !(vnew >= vb && vnew < vb + 32);
+  };
   // K of block vb: lane's rows vb+l16 and vb+16+l16, k-slot group lg
   auto load_k = [&](int vb, RawT* ka, RawT* kb) {
+    if (plain(vb)) {
+      const size_t e0 = (row0 + virt_row(vb, sp.n1, sr)) * D + (size_t)l16 * D;
+#pragma unroll
+      for (int t = 0; t < KSTEPS; ++t) {
+        const int col = 8 * (KSTEPS * lg + t);
+        ka[t] = load_raw8<FP8>(a.ck, e0 + col, true);
+        kb[t] = load_raw8<FP8>(a.ck, e0 + 16 * D + col, true);
+      }
+      return;
+    }
     const int va = vb + l16, vb2 = vb + 16 + l16;
     const void* pa = va == vnew ? a.k_new : a.ck;
     const void* pb = vb2 == vnew ? a.k_new : a.ck;
@@ -222,13 +237,23 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
     // V of this block (eight rows per lane, in the order of the score layout),
     // then K of the next block: the value product waits only for V.
     RawT vv[VPASS][8];
+    if (plain(vb)) {
+      const size_t e0 = (row0 + virt_row(vb, sp.n1, sr)) * vstride + 8 * l16;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
-      const void* pv = vi == vnew ? a.v_new : vbase;
-      const size_t ev = vi == vnew ? vnew_off : (row0 + virt_row(vi, sp.n1, sr)) * vstride;
+      for (int i = 0; i < 8; ++i) {
+        const int r = i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4);
 #pragma unroll
-      for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(pv, ev + 128 * pp + 8 * l16, vi < sp.v1);
+        for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(vbase, e0 + (size_t)r * vstride + 128 * pp, true);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
+        const void* pv = vi == vnew ? a.v_new : vbase;
+        const size_t ev = vi == vnew ? vnew_off : (row0 + virt_row(vi, sp.n1, sr)) * vstride;
+#pragma unroll
+        for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(pv, ev + 128 * pp + 8 * l16, vi < sp.v1);
+      }
     }
     RawT kn[KSTEPS], kn2[KSTEPS];
     if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
@@ -239,30 +264,45 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
       s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(ka[t])), qf[t], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(kb[t])), qf[t], s1, 0, 0, 0);
     }
+    // raw dot products; the scale (> 0, fp8 key scale included) is applied to
+    // the block max and folded into the exponent
     float x[8];
+    if (vb + 32 <= sp.v1) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
-      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        x[e] = s0[e];
+        x[4 + e] = s1[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] : -INFINITY;
+        x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] : -INFINITY;
+      }
     }
     float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
     bm = fmaxf(bm, __shfl_xor(bm, 16));
     bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float mn = fmaxf(m, bm);
-    float alpha = 1.f, pe[8];
-    if (mn == -INFINITY) {
+    bm *= xs;
+    const bool up = bm > m + kStaleMax;  // always true for the first valid block (m = -inf)
+    if (wave_any(up)) {
+      const float mnew = up ? bm : m;
+      const float alpha = up ? fast_exp2(m - mnew) : 1.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = 0.f;
-    } else {
-      alpha = fast_exp2(m - mn);
+      for (int pp = 0; pp < VPASS; ++pp)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(x[i] - mn);
+        for (int c = 0; c < 8; ++c) acc[pp][c] *= alpha;
+      lsum *= alpha;
+      m = mnew;
+      mref = m == -INFINITY ? 0.f : m;  // no valid row yet: every x is -inf, exp2 gives 0
     }
-    m = mn;
-    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    float pe[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(fmaf(x[i], xs, -mref));
+    lsum += ((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7]));
     u32x4 pw;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(pe[2 * i], pe[2 * i + 1]);
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
     for (int pp = 0; pp < VPASS; ++pp) {
@@ -276,7 +316,6 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
         u32x4 av;
 #pragma unroll
         for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vbf[2 * i + 1][u], vbf[2 * i][u], selb);
-        acc[pp][c] *= alpha;
         acc[pp][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[pp][c], 0, 0, 0);
       }
     }
@@ -323,9 +362,9 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
   constexpr int D = kMlaKSteps * 32;  // 576
   typedef typename Raw8<FP8>::T RawT;
   __shared__ f32x4 sbuf[2][4][2][64];  // [parity][wave][row set][lane]
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = tid() & 63, w = tid() >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
-  const int chunk = blockIdx.x, b = blockIdx.y;  // one KV head
+  const int chunk = bid_x(), b = bid_y();  // one KV head
   int slot;
   RowSpan sp;
   if (!span_of(a, b, chunk, slot, sp)) return;
@@ -349,7 +388,7 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
   const float ksc = FP8 ? a.k_scale[slot] : 1.f;
   const float xs = a.scale * kLog2e * ksc;
 
-  float m = -INFINITY, lsum = 0.f;
+  float m = -INFINITY, mref = 0.f, lsum = 0.f;  // reference max (log2 units), its finite stand-in, sum
   f32x4 acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -393,30 +432,43 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
     __syncthreads();
     s0 = ((sbuf[parity][0][0][lane] + sbuf[parity][1][0][lane]) + sbuf[parity][2][0][lane]) + sbuf[parity][3][0][lane];
     s1 = ((sbuf[parity][0][1][lane] + sbuf[parity][1][1][lane]) + sbuf[parity][2][1][lane]) + sbuf[parity][3][1][lane];
+    // raw dot products; the scale (> 0, fp8 key scale included) is applied to
+    // the block max and folded into the exponent
     float x[8];
+    if (vb + 32 <= sp.v1) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] * xs : -INFINITY;
-      x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] * xs : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        x[e] = s0[e];
+        x[4 + e] = s1[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] : -INFINITY;
+        x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] : -INFINITY;
+      }
     }
     float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
     bm = fmaxf(bm, __shfl_xor(bm, 16));
     bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float mn = fmaxf(m, bm);
-    float alpha = 1.f, pe[8];
-    if (mn == -INFINITY) {
+    bm *= xs;
+    const bool up = bm > m + kStaleMax;  // always true for the first valid block (m = -inf)
+    if (wave_any(up)) {
+      const float mnew = up ? bm : m;
+      const float alpha = up ? fast_exp2(m - mnew) : 1.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = 0.f;
-    } else {
-      alpha = fast_exp2(m - mn);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(x[i] - mn);
+      for (int c = 0; c < 8; ++c) acc[c] *= alpha;
+      lsum *= alpha;
+      m = mnew;
+      mref = m == -INFINITY ? 0.f : m;  // no valid row yet: every x is -inf, exp2 gives 0
     }
-    m = mn;
-    lsum = lsum * alpha + (((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7])));
+    float pe[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pe[i] = fast_exp2(fmaf(x[i], xs, -mref));
+    lsum += ((pe[0] + pe[1]) + (pe[2] + pe[3])) + ((pe[4] + pe[5]) + (pe[6] + pe[7]));
     u32x4 pw;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pw[i] = f32_to_bf16_bits(pe[2 * i]) | (f32_to_bf16_bits(pe[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(pe[2 * i], pe[2 * i + 1]);
     const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
     u32x4 vbf[8];
 #pragma unroll
@@ -428,7 +480,6 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
       u32x4 av;
 #pragma unroll
       for (int i = 0; i < 4; ++i) av[i] = __builtin_amdgcn_perm(vbf[2 * i + 1][u], vbf[2 * i][u], selb);
-      acc[c] *= alpha;
       acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb, acc[c], 0, 0, 0);
     }
 #pragma unroll
@@ -517,9 +568,9 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   constexpr int D = 576;
   __shared__ __align__(16) unsigned char stage[kLatStages][kLatBlockBytes];
   __shared__ f32x4 sx[4][2][64];  // partial logits [wave][row set][lane]
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = tid() & 63, w = tid() >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
-  const int chunk = blockIdx.x, b = blockIdx.y;
+  const int chunk = bid_x(), b = bid_y();
   int slot;
   RowSpan sp;
   if (!span_of(a, b, chunk, slot, sp)) return;
@@ -557,7 +608,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   const int vnew = new_row(a, slot);
   const unsigned char* knew = vnew >= 0 ? (const unsigned char*)a.k_new + (size_t)b * kLatRowBytes : nullptr;
   u32x4 newp = {0u, 0u, 0u, 0u};
-  const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, 0, threadIdx.x, newp);
+  const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, 0, tid(), newp);
   const int nblk = __builtin_amdgcn_readfirstlane((sp.v1 - sp.v0 + 31) / 32);
   auto issue = [&](int blk) {
     const int vb = sp.v0 + 32 * blk;
@@ -590,7 +641,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   lat_wait_vm<0>();  // query fragments (and the new row's piece) landed
   // The store is counted by vmcnt with the block loads issued after it; loads
   // complete in order, so the waits below still cover the blocks they name.
-  if (has_newp) new_piece_store(a, 0, slot, vnew, threadIdx.x, newp);
+  if (has_newp) new_piece_store(a, 0, slot, vnew, tid(), newp);
   for (int s = 0; s < kLatStages && s < nblk; ++s) issue(s);
 
   for (int i = 0; i < nblk; ++i) {
@@ -708,8 +759,8 @@ __device__ __forceinline__ float load_kv(const void* base, size_t i, float scale
 template <typename KV>
 __global__ __launch_bounds__(64) void decode_generic(DecodeArgs a) {
   constexpr int kMaxDk = 9, kMaxDv = 8;  // dk <= 576, dv <= 512
-  const int lane = threadIdx.x;
-  const int chunk = blockIdx.x, bh = blockIdx.y, b = bh / a.Hq, qh = bh % a.Hq, g = qh / a.G;
+  const int lane = tid();
+  const int chunk = bid_x(), bh = bid_y(), b = bh / a.Hq, qh = bh % a.Hq, g = qh / a.G;
   int slot;
   RowSpan sp;
   if (!span_of(a, b, chunk, slot, sp)) return;
@@ -783,13 +834,13 @@ constexpr int kCombineThreads = 128;
 __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   __shared__ float wts[kMaxChunks];
   __shared__ float red[kCombineThreads / 64];
-  const int bh = blockIdx.x, b = bh / a.Hq;
+  const int bh = bid_x(), b = bh / a.Hq;
   const int slot = a.slot_ids[b];
   if (slot < 0 || slot >= a.n_slots) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = tid() & 63, wave = tid() >> 6;
   const float2* ml = a.ml + (size_t)bh * a.n_chunks;
   float M = -INFINITY;
-  for (int c = threadIdx.x; c < a.n_chunks; c += blockDim.x) M = fmaxf(M, ml[c].x);
+  for (int c = tid(); c < a.n_chunks; c += nthreads()) M = fmaxf(M, ml[c].x);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   if (lane == 0) red[wave] = M;
@@ -798,7 +849,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   for (int i = 1; i < kCombineThreads / 64; ++i) M = fmaxf(M, red[i]);
   __syncthreads();
   float ws = 0.f;
-  for (int c = threadIdx.x; c < a.n_chunks; c += blockDim.x) {
+  for (int c = tid(); c < a.n_chunks; c += nthreads()) {
     float2 v = ml[c];
     float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : fast_exp2(v.x - M);
     wts[c] = wc;
@@ -810,7 +861,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   float wsum = 0.f;
   for (int i = 0; i < kCombineThreads / 64; ++i) wsum += red[i];
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  const int d = blockIdx.y * kCombineThreads + threadIdx.x;
+  const int d = bid_y() * kCombineThreads + tid();
   if (d >= a.dv) return;
   const float* part = a.part + (size_t)bh * a.n_chunks * a.dv + d;
   float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
@@ -877,7 +928,7 @@ __device__ __forceinline__ void put8(const In* src, Out* dst, float scale) {
 
 template <typename In, typename Out>
 __global__ __launch_bounds__(256) void append(AppendArgs a) {
-  const int b = blockIdx.x;
+  const int b = bid_x();
   const int slot = a.slot_ids[b];
   if (slot < 0 || slot >= a.n_slots) return;
   const int p = a.pos[slot];
@@ -885,7 +936,7 @@ __global__ __launch_bounds__(256) void append(AppendArgs a) {
   const int s = a.sink, r = a.recent, B = s + r + a.topk;
   const int row = p < s ? p : s + (p - s) % r;
   const int kc = a.dk / 8, vc = a.v_new ? a.dv / 8 : 0;
-  for (int i = threadIdx.x; i < a.Hkv * (kc + vc); i += blockDim.x) {
+  for (int i = tid(); i < a.Hkv * (kc + vc); i += nthreads()) {
     const int g = i / (kc + vc), c = i % (kc + vc);
     const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + row;
     if (c < kc) {
@@ -902,7 +953,7 @@ __global__ __launch_bounds__(256) void append(AppendArgs a) {
 }
 
 __global__ __launch_bounds__(256) void advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids) {
-  for (int b = threadIdx.x + blockIdx.x * blockDim.x; b < n; b += blockDim.x * gridDim.x) {
+  for (int b = tid(); b < n; b += nthreads()) {  // one workgroup
     int s = slot_ids[b];
     if (s >= 0 && s < n_slots) atomicAdd(&pos[s], 1);
   }

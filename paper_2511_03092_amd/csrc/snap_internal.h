@@ -39,6 +39,23 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
+// Work-item and workgroup indices straight from the hardware.  HIP's
+// threadIdx / blockIdx / blockDim are device-library functions that cannot be
+// inlined into kernels built without packed fp32 ops and IEEE mode (their
+// target attributes differ), so they would become real calls whose results
+// the compiler must treat as divergent.
+__device__ __forceinline__ int tid() { return (int)__builtin_amdgcn_workitem_id_x(); }
+__device__ __forceinline__ int bid_x() { return (int)__builtin_amdgcn_workgroup_id_x(); }
+__device__ __forceinline__ int bid_y() { return (int)__builtin_amdgcn_workgroup_id_y(); }
+__device__ __forceinline__ int nthreads() { return (int)__builtin_amdgcn_workgroup_size_x(); }
+
+// A workgroup-uniform value read from global memory.  Kernels that also write
+// global memory read their metadata with vector loads (the scalar cache is not
+// coherent with those writes), which leaves the value in a vector register and
+// makes the compiler treat control flow that depends on it as divergent;
+// readfirstlane moves it back to a scalar register.
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 // true when pred holds in any lane of the wave (wave-uniform)
 __device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
 
