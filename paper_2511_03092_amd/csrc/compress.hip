@@ -127,6 +127,9 @@ __device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c
 // kept in log2 units, y = <q,k> * scale * log2(e), formed by one rounded
 // multiply, so exp(z) = exp2(y).  `interior` (uniform) means every key of the
 // tile is a candidate that precedes every window row: no per-element masks.
+// LDS fragment reads issued ahead of their MFMAs (measured: 4 is 4% faster
+// than the scheduler's own 2 on the latent shape; 6 is no better).
+constexpr int kReadAhead = 4;
 template <typename In, int KSTEPS, int NW, bool COLSUM>
 __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned char* __restrict__ ktile,
                                            const bf16x8 (&qf)[2][KSTEPS], const float* qlds, float* colbuf,
@@ -157,6 +160,15 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
           acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
         }
       }
+      // the fragment reads run kReadAhead k-steps ahead of the MFMAs that use
+      // them, so their LDS latency hides behind earlier products
+      __builtin_amdgcn_sched_group_barrier(0x100, kReadAhead, 0);  // DS reads
+#pragma unroll
+      for (int t = 0; t < KSTEPS - kReadAhead; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * kReadAhead, 0);
       acc[0] += odd[0];
       acc[1] += odd[1];
     } else if (wave_has_rows) {
@@ -868,13 +880,17 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   g.rows = G * p.obs_window;
   g.rows_pad = (g.rows + 31) / 32 * 32;
   int groups = n_seq * p.n_kv_heads;
-  // enough workgroups to cover 256 CUs several times, at most 4096 keys each
+  // Key chunks: enough workgroups to cover the 256 CUs several times (about
+  // 4096), but each chunk at least 16 * rows_pad keys, so that its keys
+  // outweigh the query fragments every workgroup loads first by 16x (the
+  // 256-row latent shape: 4096-key chunks; 128-row GQA: 2048).
   long target = 4096;
   long per_group = (target + groups - 1) / (groups > 0 ? groups : 1);
   long kc = (max_len + per_group - 1) / (per_group > 0 ? per_group : 1);
+  const long kc_min = 16L * g.rows_pad;
+  if (kc < kc_min) kc = kc_min;
   kc = (kc + kKeyTile - 1) / kKeyTile * kKeyTile;
-  if (kc < kKeyTile) kc = kKeyTile;
-  if (kc > 4096) kc = 4096;
+  if (kc > 16384) kc = 16384;
   g.key_chunk = (int)kc;
   g.n_kchunks = (int)((max_len + kc - 1) / kc);
   if (g.n_kchunks < 1) g.n_kchunks = 1;
