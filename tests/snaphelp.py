@@ -114,9 +114,7 @@ def expected_cache(L, s, r, K, x, sel):
 def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gsel, gpooled):
     """Full check of one compress call.  Returns the tolerated swaps, the max
     relative error of the pooled scores over all candidates, and over the
-    decision band (oracle score within a factor 4 of the K-th largest): a band
-    error <= 5e-7 means no two candidates can trade places unless their exact
-    scores differ by less than 1e-6."""
+    decision band (oracle score within a factor 4 of the K-th largest)."""
     op = oracle_params(p)
     res = oracle.compress(op, lengths, q, k, v)
     ck, cv = cache.host_values()

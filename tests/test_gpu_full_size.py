@@ -147,3 +147,100 @@ def test_mla_workload_one_layer_full_size():
     _structural(p, k, v, cache, sel, pooled, lengths)
     _oracle_units(p, q, k, v, cache, sel, pooled, lengths, [(5, 0)])
     _decode_check(p, wl, cache, 2, [0, 5, 15])
+
+
+def test_cb_fp8_workload_full_size():
+    """The continuous-batching shape: 8 prompts of the workload's length mix
+    (4k-128k) compressed into 8 of the 32 fp8 slots, per-(slot, head) scales
+    = amax / 448.  Every unit: metadata, index-set structure, zero padding.
+    Sampled units: selection and every fp8 code against the oracle's
+    quantisation of the oracle's assembly.  Then two fused decode steps,
+    checked against the oracle on the GPU's cache bytes for three slots."""
+    wl = synth.WORKLOADS["cb-fp8-llama8b-32slot"]
+    slots = [3, 17, 0, 31, 8, 22, 12, 5]
+    lengths = synth.draw_lengths(wl, 0, len(slots))
+    _announce(f"cb-fp8-llama8b-32slot at full size: lengths {lengths} into slots {slots} of {wl.slots}")
+    p = params_of(wl)
+    s, r, K = p.sink, p.recent, p.topk
+    max_len = max(lengths)
+    q, k, v = synth.prefill_batch(wl, 0, lengths, device="cuda", max_len=max_len, pad_value=float("nan"),
+                                  slots=slots)
+    cache = GpuCache(p, wl.slots)
+    for b, s_ in enumerate(slots):
+        L = lengths[b]
+        cache.k_scale[s_] = k[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0
+        cache.v_scale[s_] = v[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0
+    n = len(slots)
+    sl = torch.tensor(slots, dtype=torch.int32, device="cuda")
+    lens = torch.tensor(lengths, dtype=torch.int32, device="cuda")
+    ws = snap.workspace(snap.snap_compress_workspace(p, n, max_len))
+    sel = torch.empty((n, p.n_kv_heads, K), dtype=torch.int32, device="cuda")
+    pooled = torch.empty((n, p.n_kv_heads, max_len), dtype=torch.float32, device="cuda")
+    snap.snap_compress(p, cache.c(), cache.pos, cache.n_topk, sl, lens, q, k, v, ws, sel, pooled)
+    torch.cuda.synchronize()
+
+    pos, nt = cache.pos.cpu().tolist(), cache.n_topk.cpu().tolist()
+    for b, L in enumerate(lengths):
+        keff = min(max(L - s - r, 0), K)
+        assert pos[slots[b]] == L and nt[slots[b]] == keff
+        S = sel[b]
+        assert torch.all(S[:, keff:] == -1)
+        assert torch.all(S[:, 1:keff] > S[:, :keff - 1]) and int(S[:, :keff].min()) >= s
+        assert int(S[:, :keff].max()) < L - r
+        assert torch.all(cache.k[slots[b], :, s + r + keff:] == 0)
+        assert torch.all(cache.v[slots[b], :, s + r + keff:] == 0)
+    untouched = [x for x in range(wl.slots) if x not in slots]
+    assert torch.all(cache.pos[untouched] == -1)
+
+    op = oracle_params(p)
+    G = op.group
+    units = [(int(np.argmax(lengths)), 0), (int(np.argmin(lengths)), 7), (2, 3)]
+
+    def run(u):
+        b, g = u
+        L = lengths[b]
+        return u, oracle.compress_group(op, L, oracle.f64(q[b, g * G:(g + 1) * G]), oracle.f64(k[b, g, :L]),
+                                        oracle.f64(v[b, g, :L]))
+
+    with ThreadPoolExecutor(len(units)) as ex:
+        results = list(ex.map(run, units))
+    worst_band = 0.0
+    for (b, g), res in results:
+        L, s_ = lengths[b], slots[b]
+        keff = min(max(L - s - r, 0), K)
+        gs = sel[b, g].cpu().numpy()
+        swaps = check_selection(gs, res.P, L, s, r, K, SEL_RTOL)
+        for src, dst, sc in ((k, cache.k, cache.k_scale), (v, cache.v, cache.v_scale)):
+            rows = oracle.assemble(L, s, r, K, oracle.f64(src[b, g, :L]), gs[:keff])
+            codes = oracle.quantize(rows, float(sc[s_, g])).reshape(rows.shape)
+            assert np.array_equal(dst[s_, g].cpu().numpy(), codes), (b, g)
+        c = slice(s, L - r)
+        gp = pooled[b, g, c].double().cpu().numpy()
+        rel = np.abs(gp - res.P[c]) / np.maximum(res.P[c], 1e-30)
+        tau = np.sort(res.P[c])[::-1][keff - 1]
+        band = (res.P[c] >= tau / 4) & (res.P[c] <= 4 * tau)
+        worst_band = max(worst_band, float(rel[band].max()))
+        print(f"  unit (seq {b} -> slot {s_}, head {g}, L={L}): swaps {swaps}, band rel err {rel[band].max():.3e}",
+              flush=True)
+    assert worst_band <= BAND_RTOL
+
+    dws = snap.workspace(snap.snap_decode_workspace(p, n))
+    out = torch.empty((n, p.n_q_heads, p.d_v), dtype=torch.bfloat16, device="cuda")
+    worst = 0.0
+    for step in range(2):
+        positions = cache.pos[sl.long()].cpu().tolist()
+        qd, kn, vn = synth.decode_inputs(wl, 0, step, positions, device="cuda")
+        snap.snap_decode_step(p, cache.c(), cache.pos, cache.n_topk, sl, qd, kn, vn, out, dws)
+        snap.snap_advance(cache.pos, sl)
+        torch.cuda.synchronize()
+        ntv = cache.n_topk.cpu().numpy()
+        for i in (0, 3, 6):
+            s_ = slots[i]
+            table = torch.tensor([oracle.e4m3_value(x) for x in range(256)], dtype=torch.float64)
+            ck = (table[cache.k[s_].cpu().long()] * cache.k_scale[s_].cpu().double()[:, None, None]).numpy()
+            cv = (table[cache.v[s_].cpu().long()] * cache.v_scale[s_].cpu().double()[:, None, None]).numpy()
+            exp = oracle.decode_attn(op, [positions[i]], ntv[[s_]], qd[i:i + 1].cpu(), ck[None], cv[None])
+            err = float(np.max(np.abs(out[i:i + 1].double().cpu().numpy() - exp)))
+            worst = max(worst, err)
+            assert err <= TOL["fp8"], (step, s_, err)
+    print(f"  decode max abs err: {worst:.3e}", flush=True)
