@@ -584,15 +584,6 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   // dims 32*kb + 8*(kc*lg + t), t < kc
   const int kb = mla_kbeg(wu), kc = mla_kcnt(wu);
   bf16x8 qf[5];
-  {
-    const uint16_t* qp = (const uint16_t*)a.q + ((size_t)b * a.Hq + (hval ? h : 0)) * D;
-#pragma unroll
-    for (int t = 0; t < 5; ++t) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (hval && t < kc) v = *(const u32x4*)(qp + 32 * kb + 8 * (kc * lg + t));
-      qf[t] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
   // this lane's share of every block load: (row, chunk) of its 9 slots
   int ld_r[kLatLoadsPerWave], ld_c[kLatLoadsPerWave], ld_off[kLatLoadsPerWave];
 #pragma unroll
@@ -638,11 +629,39 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  lat_wait_vm<0>();  // query fragments (and the new row's piece) landed
-  // The store is counted by vmcnt with the block loads issued after it; loads
-  // complete in order, so the waits below still cover the blocks they name.
-  if (has_newp) new_piece_store(a, 0, slot, vnew, tid(), newp);
-  for (int s = 0; s < kLatStages && s < nblk; ++s) issue(s);
+  // Prologue: the query rows (G x 1152 bytes) go straight to LDS in the last
+  // stage, ahead of blocks 0..2, so one wait covers both and the first block
+  // lands after a single memory latency.  Once every wave has copied its
+  // query fragments out, the last stage takes block 3.
+  if (nblk > 0) {
+    const int qchunks = a.G * kLatChunks;
+    const int nq = (qchunks + 63) / 64;  // wave-instructions (G <= 16: at most 18)
+    const unsigned char* qsrc = (const unsigned char*)a.q + (size_t)b * a.Hq * kLatRowBytes;
+    unsigned char* qdst = &stage[kLatStages - 1][0];
+    for (int ii = wu; ii < nq; ii += 4) {
+      int qc = ii * 64 + lane;
+      qc = qc < qchunks ? qc : 0;  // the last instruction's spare lanes re-read chunk 0
+      dma16_lat(qsrc + (size_t)qc * 16, qdst + (size_t)ii * 1024);
+    }
+    const int pro = min(nblk, kLatStages - 1);
+    for (int s = 0; s < pro; ++s) issue(s);
+    // block 0 (and every older load: the query) has landed
+    if (pro == 3)
+      lat_wait_vm<2 * kLatLoadsPerWave>();
+    else if (pro == 2)
+      lat_wait_vm<kLatLoadsPerWave>();
+    else
+      lat_wait_vm<0>();
+    lat_barrier();
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (hval && t < kc) v = *(const u32x4*)(qdst + (size_t)h * kLatRowBytes + (32 * kb + 8 * (kc * lg + t)) * 2);
+      qf[t] = __builtin_bit_cast(bf16x8, v);
+    }
+    lat_barrier();  // every wave has its query fragments: the last stage is free
+    if (nblk > kLatStages - 1) issue(kLatStages - 1);
+  }
 
   for (int i = 0; i < nblk; ++i) {
     const int after = min(nblk - 1 - i, kLatStages - 1);  // block loads issued after block i
@@ -733,6 +752,9 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   }
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
+  // the new row's store waits until here: its load is then long done, and no
+  // other workgroup of this launch reads that row
+  if (has_newp) new_piece_store(a, 0, slot, vnew, tid(), newp);
   if (!hval) return;
   const size_t pi = ((size_t)b * a.Hq + h) * a.n_chunks + chunk;
   if (w == 0 && lg == 0) a.ml[pi] = make_float2(m, lsum);
