@@ -37,11 +37,14 @@ struct ScoreArgs {
   float scale2_lo;  // scale * log2(e) - scale2
 };
 
-// LDS tile of kKeyTile = 64 keys stored chunk-major: the 16-byte chunk c of key
-// k sits at slot c*64 + k.  A fragment read by 16 consecutive keys of one
-// chunk is 256 contiguous bytes (all 64 banks once), and in every tile load
-// lane = key, so a lane needs one row pointer and the chunk offset is uniform.
-__device__ __forceinline__ int tile_slot(int key, int c) { return c * kKeyTile + key; }
+// LDS tile of TK keys (64, or 32 for 576-wide rows) stored chunk-major: the
+// 16-byte chunk c of key k sits at slot c*TK + k.  A fragment read by 16
+// consecutive keys of one chunk is 256 contiguous bytes, and every tile load
+// instruction covers 64 consecutive slots (lane i -> slot base + i).  (A
+// row-major tile with a swizzled chunk index, whose loads read contiguous
+// memory, measured slower for both row widths.)
+template <int TK>
+__device__ __forceinline__ int tile_slot(int key, int c) { return c * TK + key; }
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 
@@ -52,7 +55,9 @@ typedef __attribute__((address_space(3))) void* lds_void_ptr;
 // tile in flight).  M0 (the LDS base of the DMA) is saved and restored, with
 // the one wait state an M0 write needs before an LDS DMA.
 __device__ __forceinline__ void dma16(const void* g, const void* lds_wave_base) {
-  const uint32_t la = (uint32_t)(uintptr_t)(lds_void_ptr)lds_wave_base;
+  // wave-uniform by construction; readfirstlane keeps it in a scalar register
+  // whatever the compiler's uniformity analysis concludes
+  const uint32_t la = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)lds_wave_base);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -66,24 +71,49 @@ __device__ __forceinline__ void dma16(const void* g, const void* lds_wave_base) 
       : "memory");
 }
 
-// Issue this wave's share of one key tile: CPR wave-instructions per tile
-// (chunk c = wave + ii*NW), each moving 64 x 16 bytes straight into LDS (no
-// VGPRs).  Keys past c1 read key c1-1 instead so every wave always issues the
-// same number of loads (those bytes are never used).
-template <int CPR, int NW>
+// Issue this wave's share of one key tile: the tile is CPR*TK/64
+// wave-instructions, each moving 64 x 16 bytes straight into LDS (no VGPRs);
+// wave w issues instructions w, w+NW, ...  Keys past c1 read key c1-1
+// instead, so a wave always issues the same number of loads per tile (those
+// bytes are never used).
+template <int CPR, int NW, int TK>
 __device__ __forceinline__ void issue_tile(const unsigned char* kbase, size_t row_bytes, int t0, int c1,
                                            unsigned char* buf, int wave, int lane) {
-  static_assert(CPR % NW == 0, "tile loads must split evenly over the waves");
-  static_assert(kKeyTile == 64, "one key per lane");
-  int j = t0 + lane;
-  j = j < c1 ? j : c1 - 1;
-  const unsigned char* rowp = kbase + (size_t)j * row_bytes;
+  constexpr int NI = CPR * TK / 64;
+  constexpr int KMAX = (NI + NW - 1) / NW;  // loads of the busiest wave
+  static_assert(CPR * TK % 64 == 0, "a tile is a whole number of wave-instructions");
   const int w = __builtin_amdgcn_readfirstlane(wave);
+  if constexpr (TK == 64) {
+    // one key per lane: a single row pointer, chunk c = instruction index
+    int j = t0 + lane;
+    j = j < c1 ? j : c1 - 1;
+    const unsigned char* rowp = kbase + (size_t)j * row_bytes;
 #pragma unroll
-  for (int ii = 0; ii < CPR / NW; ++ii) {
-    const int c = w + ii * NW;
-    dma16(rowp + c * 16, buf + (size_t)c * 1024);
+    for (int k = 0; k < KMAX; ++k) {
+      const int c = w + k * NW;
+      if (NI % NW != 0 && c >= NI) break;  // wave-uniform
+      dma16(rowp + c * 16, buf + (size_t)c * 1024);
+    }
+  } else {
+    // 64 / TK chunks per instruction: lane -> (chunk, key)
+    const unsigned ul = (unsigned)lane;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const int ii = w + k * NW;
+      if (NI % NW != 0 && ii >= NI) break;  // wave-uniform
+      const unsigned slot = (unsigned)ii * 64u + ul;
+      const int c = (int)(slot / TK), key = (int)(slot % TK);
+      int j = t0 + key;
+      j = j < c1 ? j : c1 - 1;
+      dma16(kbase + (size_t)j * row_bytes + c * 16, buf + (size_t)ii * 1024);
+    }
   }
+}
+// this wave's loads per tile
+template <int CPR, int NW, int TK>
+__device__ __forceinline__ int tile_loads(int wave) {
+  constexpr int NI = CPR * TK / 64;
+  return (NI - wave + NW - 1) / NW;
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight.
@@ -92,6 +122,25 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N < 64, "vmcnt field");
   // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// vmcnt <= n for a wave-uniform n (a switch over the encodings; n > 24
+// falls back to waiting for everything, which is always safe)
+__device__ __forceinline__ void wait_vm_dyn(int n) {
+  switch (n) {
+#define SNAP_WAIT_CASE(N) \
+  case N:                 \
+    wait_vm<N>();         \
+    break;
+    SNAP_WAIT_CASE(0) SNAP_WAIT_CASE(1) SNAP_WAIT_CASE(2) SNAP_WAIT_CASE(3) SNAP_WAIT_CASE(4)
+    SNAP_WAIT_CASE(5) SNAP_WAIT_CASE(6) SNAP_WAIT_CASE(7) SNAP_WAIT_CASE(8) SNAP_WAIT_CASE(9)
+    SNAP_WAIT_CASE(10) SNAP_WAIT_CASE(11) SNAP_WAIT_CASE(12) SNAP_WAIT_CASE(13) SNAP_WAIT_CASE(14)
+    SNAP_WAIT_CASE(15) SNAP_WAIT_CASE(16) SNAP_WAIT_CASE(17) SNAP_WAIT_CASE(18) SNAP_WAIT_CASE(19)
+    SNAP_WAIT_CASE(20) SNAP_WAIT_CASE(21) SNAP_WAIT_CASE(22) SNAP_WAIT_CASE(23) SNAP_WAIT_CASE(24)
+#undef SNAP_WAIT_CASE
+    default:
+      wait_vm<0>();
+      break;
+  }
 }
 
 // Workgroup barrier that waits only for this wave's LDS traffic (not for its
@@ -130,18 +179,19 @@ __device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c
 // LDS fragment reads issued ahead of their MFMAs (measured: 4 is 4% faster
 // than the scheduler's own 2 on the latent shape; 6 is no better).
 constexpr int kReadAhead = 4;
-template <typename In, int KSTEPS, int NW, bool COLSUM>
+template <typename In, int KSTEPS, int NW, bool COLSUM, int TK>
 __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned char* __restrict__ ktile,
                                            const bf16x8 (&qf)[2][KSTEPS], const float* qlds, float* colbuf,
                                            ScoreLane& sl, int t0, int c1, bool interior, int bg, int wave,
                                            int lane, bool wave_has_rows) {
   constexpr bool kBF16 = sizeof(In) == 2;
   constexpr int D = KSTEPS * 32;
+  static_assert(TK == 64 || TK == 32, "tile of 64 or 32 keys");
   const int l16 = lane & 15, lg = lane >> 4;
   const float s2 = a.scale2, s2lo = a.scale2_lo;
-  float xv[2][4][kKeyTile / 16];
+  float xv[2][4][TK / 16];
 #pragma unroll
-  for (int sb = 0; sb < kKeyTile / 16; ++sb) {
+  for (int sb = 0; sb < TK / 16; ++sb) {
     f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
     const int key = sb * 16 + l16;
     if constexpr (kBF16) {
@@ -151,7 +201,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
       f32x4 odd[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int t = 0; t < KSTEPS; ++t) {
-        bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot(key, KSTEPS * lg + t) * 16));
+        bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot<TK>(key, KSTEPS * lg + t) * 16));
         if (t & 1) {
           odd[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, odd[0], 0, 0, 0);
           odd[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, odd[1], 0, 0, 0);
@@ -181,7 +231,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
           double sacc = 0.0;
 #pragma unroll 4
           for (int d = 0; d < D; ++d) {
-            const float kd = *(const float*)(ktile + (size_t)tile_slot(key, d >> 2) * 16 + (d & 3) * 4);
+            const float kd = *(const float*)(ktile + (size_t)tile_slot<TK>(key, d >> 2) * 16 + (d & 3) * 4);
             sacc = fma((double)qrow[d], (double)kd, sacc);
           }
           acc[rb][e] = (float)sacc;
@@ -220,7 +270,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
                  ((colv[1][0] + colv[1][1]) + (colv[1][2] + colv[1][3]));
       cs += __shfl_xor(cs, 16);
       cs += __shfl_xor(cs, 32);
-      if (lg == 0) colbuf[wave * kKeyTile + sb * 16 + l16] = cs;
+      if (lg == 0) colbuf[wave * TK + sb * 16 + l16] = cs;
     }
   }
   if (!COLSUM) {
@@ -228,25 +278,34 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float mt = fmaxf(fmaxf(xv[rb][e][0], xv[rb][e][1]), fmaxf(xv[rb][e][2], xv[rb][e][3]));
-        float mn = fmaxf(sl.rm[rb][e], mt);
+        const float* x = xv[rb][e];
+        float mt, mn;
+        if constexpr (TK == 64) {
+          mt = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+        } else {
+          mt = fmaxf(x[0], x[1]);
+        }
+        mn = fmaxf(sl.rm[rb][e], mt);
         if (mn == -INFINITY) continue;
         float z = sl.rz[rb][e] * fast_exp2(sl.rm[rb][e] - mn);
-        z += (fast_exp2(xv[rb][e][0] - mn) + fast_exp2(xv[rb][e][1] - mn)) + (fast_exp2(xv[rb][e][2] - mn) + fast_exp2(xv[rb][e][3] - mn));
+        if constexpr (TK == 64) {
+          z += (fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) + (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn));
+        } else {
+          z += fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn);
+        }
         sl.rz[rb][e] = z;
         sl.rm[rb][e] = mn;
       }
   } else {
     lds_barrier();
-    if (tid() < kKeyTile) {
+    if (tid() < TK) {
       int j = t0 + tid();
       const float* c = colbuf + tid();
       float sum;
       if constexpr (NW == 4) {
-        sum = (c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile]);
+        sum = (c[0] + c[TK]) + (c[2 * TK] + c[3 * TK]);
       } else {
-        sum = ((c[0] + c[kKeyTile]) + (c[2 * kKeyTile] + c[3 * kKeyTile])) +
-              ((c[4 * kKeyTile] + c[5 * kKeyTile]) + (c[6 * kKeyTile] + c[7 * kKeyTile]));
+        sum = ((c[0] + c[TK]) + (c[2 * TK] + c[3 * TK])) + ((c[4 * TK] + c[5 * TK]) + (c[6 * TK] + c[7 * TK]));
       }
       if (j < c1) a.A[(size_t)bg * a.max_len + j] = sum;
     }
@@ -255,20 +314,19 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
 
 // Row state of one lane: the MFMA 16x16 output gives lane l the rows
 // 4*(l/16)+e (e = 0..3) of each 16-row block and the key column l%16.
-// NW waves per workgroup; wave w owns score rows [32w, 32w+32).  Key tiles
-// are double-buffered in two LDS arrays (the loop is unrolled by two so each
-// half reads one array while the loads of the next tile fill the other).
-template <typename In, int KSTEPS, int NW, bool COLSUM>
+// NW waves per workgroup; wave w owns score rows [32w, 32w+32).  Key tiles of
+// TK keys stream through a ring of STAGES LDS stages with direct loads: while
+// a tile is scored, the next STAGES-1 are in flight (the bytes in flight per
+// CU, not the compute, bound a pass with fewer stages).
+template <typename In, int KSTEPS, int NW, bool COLSUM, int TK, int STAGES>
 __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
   constexpr bool kBF16 = sizeof(In) == 2;
   constexpr int D = KSTEPS * 32;
   constexpr int kRowBytes = D * (int)sizeof(In);
   constexpr int CPR = kRowBytes / 16;                 // 16-byte chunks per key row
-  constexpr int kTileBytes = kKeyTile * kRowBytes;
-  constexpr int IPW = CPR / NW;                        // tile loads per wave
-  __shared__ __align__(16) unsigned char tile0[kTileBytes];
-  __shared__ __align__(16) unsigned char tile1[kTileBytes];
-  __shared__ float colbuf[NW * kKeyTile];
+  constexpr int kTileBytes = TK * kRowBytes;
+  __shared__ __align__(16) unsigned char tiles[STAGES][kTileBytes];
+  __shared__ float colbuf[NW * TK];
   __shared__ float qlds[kBF16 ? 1 : 128 * D];           // fp32 inputs: [rows_pad <= 128][D]
 
   const int lane = tid() & 63, wave = tid() >> 6;
@@ -351,41 +409,66 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
       }
     }
   // The query fragments and row normalisers must have landed before the first
-  // tile load is issued: the loop's waits only count tile loads.
+  // tile load is issued: the loop's waits only count tile loads (stores issued
+  // later only add to the count, which makes those waits stricter).
   wait_vm<0>();
-  issue_tile<CPR, NW>(kbase, kRowBytes, c0, c1, tile0, wave, lane);
+  const int nt = (c1 - c0 + TK - 1) / TK;  // tiles of this chunk
+  const int nload = tile_loads<CPR, NW, TK>(__builtin_amdgcn_readfirstlane(wave));
+  // prologue: tile 0 (the double buffer issues each next tile inside its
+  // loop), or the first STAGES tiles of the ring
+  for (int st = 0; st < (STAGES == 2 ? 1 : STAGES) && st < nt; ++st)
+    issue_tile<CPR, NW, TK>(kbase, kRowBytes, c0 + st * TK, c1, &tiles[st][0], wave, lane);
 
   // a tile is interior when all its keys are in range and precede the first
   // window position (rows of negative position exist only when L < w)
   const int first_row_pos = L - a.w;
-  auto interior_of = [&](int t) { return t + kKeyTile <= c1 && t + kKeyTile - 1 <= first_row_pos; };
+  auto interior_of = [&](int t) { return t + TK <= c1 && t + TK - 1 <= first_row_pos; };
 
-  // two tiles per iteration: tile0 <- even tiles, tile1 <- odd tiles
-  for (int t0 = c0; t0 < c1; t0 += 2 * kKeyTile) {
-    {
-      lds_barrier();  // every wave is done reading tile1
-      if (t0 + kKeyTile < c1) {
-        issue_tile<CPR, NW>(kbase, kRowBytes, t0 + kKeyTile, c1, tile1, wave, lane);
-        wait_vm<IPW>();
-      } else {
-        wait_vm<0>();
+  if constexpr (STAGES == 2) {
+    // double buffer, unrolled by two (tile0 <- even tiles, tile1 <- odd
+    // tiles): the next tile is issued just before the current one is waited
+    // for.  Measured faster than the general ring for the small-row shapes.
+    constexpr int IPW = CPR * TK / 64 / NW;
+    static_assert(CPR * TK / 64 % NW == 0, "equal loads per wave");
+    unsigned char* tile0 = &tiles[0][0];
+    unsigned char* tile1 = &tiles[1][0];
+    for (int t0 = c0; t0 < c1; t0 += 2 * TK) {
+      {
+        lds_barrier();  // every wave is done reading tile1
+        if (t0 + TK < c1) {
+          issue_tile<CPR, NW, TK>(kbase, kRowBytes, t0 + TK, c1, tile1, wave, lane);
+          wait_vm<IPW>();
+        } else {
+          wait_vm<0>();
+        }
+        lds_barrier();  // tile0 holds keys [t0, t0+TK)
+        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile0, qf, qlds, colbuf, sl, t0, c1, interior_of(t0), bg, wave,
+                                               lane, wave_has_rows);
       }
-      lds_barrier();  // tile0 holds keys [t0, t0+64)
-      score_tile<In, KSTEPS, NW, COLSUM>(a, tile0, qf, qlds, colbuf, sl, t0, c1, interior_of(t0), bg, wave, lane,
-                                         wave_has_rows);
+      const int t1 = t0 + TK;
+      if (t1 < c1) {
+        lds_barrier();  // every wave is done reading tile0
+        if (t1 + TK < c1) {
+          issue_tile<CPR, NW, TK>(kbase, kRowBytes, t1 + TK, c1, tile0, wave, lane);
+          wait_vm<IPW>();
+        } else {
+          wait_vm<0>();
+        }
+        lds_barrier();  // tile1 holds keys [t1, t1+TK)
+        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile1, qf, qlds, colbuf, sl, t1, c1, interior_of(t1), bg, wave,
+                                               lane, wave_has_rows);
+      }
     }
-    const int t1 = t0 + kKeyTile;
-    if (t1 < c1) {
-      lds_barrier();  // every wave is done reading tile0
-      if (t1 + kKeyTile < c1) {
-        issue_tile<CPR, NW>(kbase, kRowBytes, t1 + kKeyTile, c1, tile0, wave, lane);
-        wait_vm<IPW>();
-      } else {
-        wait_vm<0>();
-      }
-      lds_barrier();  // tile1 holds keys [t1, t1+64)
-      score_tile<In, KSTEPS, NW, COLSUM>(a, tile1, qf, qlds, colbuf, sl, t1, c1, interior_of(t1), bg, wave, lane,
-                                         wave_has_rows);
+  } else {
+    for (int i = 0; i < nt; ++i) {
+      wait_vm_dyn(min(nt - 1 - i, STAGES - 1) * nload);  // tile i has landed
+      lds_barrier();                                      // ... for every wave
+      const int t = c0 + i * TK;
+      unsigned char* ktile = &tiles[i % STAGES][0];
+      score_tile<In, KSTEPS, NW, COLSUM, TK>(a, ktile, qf, qlds, colbuf, sl, t, c1, interior_of(t), bg, wave,
+                                             lane, wave_has_rows);
+      lds_barrier();  // every wave is done with this stage (and with colbuf)
+      if (i + STAGES < nt) issue_tile<CPR, NW, TK>(kbase, kRowBytes, t + STAGES * TK, c1, ktile, wave, lane);
     }
   }
 
@@ -918,31 +1001,36 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   return g;
 }
 
-template <typename In, int KS, int NW>
+template <typename In, int KS, int NW, int TK, int STAGES>
 static hipError_t launch_score_nw(const ScoreArgs& sa, bool colsum, int groups, int n_kchunks, hipStream_t st) {
   dim3 grid(n_kchunks, groups), block(64 * NW);
   if (colsum)
-    hipLaunchKernelGGL((score_pass<In, KS, NW, true>), grid, block, 0, st, sa);
+    hipLaunchKernelGGL((score_pass<In, KS, NW, true, TK, STAGES>), grid, block, 0, st, sa);
   else
-    hipLaunchKernelGGL((score_pass<In, KS, NW, false>), grid, block, 0, st, sa);
+    hipLaunchKernelGGL((score_pass<In, KS, NW, false, TK, STAGES>), grid, block, 0, st, sa);
   return hipGetLastError();
 }
 
-// Waves per workgroup: 4 while the score rows fit in 128, else 8.
+// Waves per workgroup: 4 while the score rows fit in 128, else 8.  Tiles and
+// stages per shape, as measured: the 576-wide latent rows take 32-key tiles in
+// 4 stages (147 KB, one workgroup per CU: three tiles in flight while one is
+// scored; 8% faster than two 64-key stages); 64/128-wide bf16 rows keep two
+// 64-key stages (three workgroups per CU; three or four stages measured
+// slower); fp32 rows 3 or 2 stages next to their fp32 query block.
 template <typename In>
 static hipError_t launch_score(const ScoreArgs& sa, int dk, bool colsum, int groups, int n_kchunks, hipStream_t st) {
   const bool wide = sa.rows_pad > 128;
   if constexpr (sizeof(In) == 2) {
-    if (dk == 64) return wide ? launch_score_nw<In, 2, 8>(sa, colsum, groups, n_kchunks, st)
-                              : launch_score_nw<In, 2, 4>(sa, colsum, groups, n_kchunks, st);
-    if (dk == 128) return wide ? launch_score_nw<In, 4, 8>(sa, colsum, groups, n_kchunks, st)
-                               : launch_score_nw<In, 4, 4>(sa, colsum, groups, n_kchunks, st);
-    if (dk == 576) return wide ? launch_score_nw<In, 18, 8>(sa, colsum, groups, n_kchunks, st)
-                               : launch_score_nw<In, 18, 4>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 64) return wide ? launch_score_nw<In, 2, 8, 64, 2>(sa, colsum, groups, n_kchunks, st)
+                              : launch_score_nw<In, 2, 4, 64, 2>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 128) return wide ? launch_score_nw<In, 4, 8, 64, 2>(sa, colsum, groups, n_kchunks, st)
+                               : launch_score_nw<In, 4, 4, 64, 2>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 576) return wide ? launch_score_nw<In, 18, 8, 32, 4>(sa, colsum, groups, n_kchunks, st)
+                               : launch_score_nw<In, 18, 4, 32, 4>(sa, colsum, groups, n_kchunks, st);
   } else {
     if (wide) return hipErrorInvalidValue;  // fp32 inputs: at most 128 score rows
-    if (dk == 64) return launch_score_nw<In, 2, 4>(sa, colsum, groups, n_kchunks, st);
-    if (dk == 128) return launch_score_nw<In, 4, 4>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 64) return launch_score_nw<In, 2, 4, 64, 3>(sa, colsum, groups, n_kchunks, st);
+    if (dk == 128) return launch_score_nw<In, 4, 4, 64, 2>(sa, colsum, groups, n_kchunks, st);
   }
   return hipErrorInvalidValue;
 }

@@ -539,7 +539,9 @@ typedef __attribute__((address_space(3))) void* lds_void_ptr_t;
 // with later LDS reads is the caller's explicit vmcnt wait and barrier.  M0
 // (the DMA's LDS base) is saved and restored around it.
 __device__ __forceinline__ void dma16_lat(const void* g, const void* lds_wave_base) {
-  const uint32_t la = (uint32_t)(uintptr_t)(lds_void_ptr_t)lds_wave_base;
+  // wave-uniform by construction; readfirstlane keeps it in a scalar register
+  // whatever the compiler's uniformity analysis concludes
+  const uint32_t la = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr_t)lds_wave_base);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"

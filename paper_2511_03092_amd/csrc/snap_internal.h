@@ -112,7 +112,7 @@ struct Geometry {
   size_t decode_bytes;
 };
 
-constexpr int kKeyTile = 64;      // keys staged in LDS per score-pass iteration
+constexpr int kKeyTile = 64;      // key chunks of the score passes are multiples of this
 constexpr int kCandChunk = 2048;  // candidates per pool/select workgroup
 constexpr int kSelThreads = 256;
 constexpr int kRadixBins = 2048;
