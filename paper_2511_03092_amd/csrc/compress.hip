@@ -10,9 +10,11 @@
 //                       the reset of the selection scratch
 //   score_pass<COLSUM>  recompute the scores, W = exp(z - c) * inv, column
 //                       sums over the G*w window rows -> A[j]
-//   pool_hist0          P = pool(A) over the candidates, first radix digit
-//   radix_pass x2       remaining digits of the K-th largest P (LDS histograms,
-//                       the last workgroup of a group picks the bin)
+//   pool_hist0          P = pool(A) over the candidates, histogram of the
+//                       first radix digit
+//   radix_scan x3       per (seq, KV head): pick the bin holding the K-th
+//                       largest P for the digit just counted
+//   radix_pass x2       histograms of the remaining digits (LDS per wave)
 //   select_count/write  ordered compaction: P > t, plus the lowest-index ties
 //   assemble            sinks, ring rows, kept rows, zero padding (+ fp8)
 #include <float.h>

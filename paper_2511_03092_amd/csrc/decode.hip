@@ -3,13 +3,19 @@
 // over the valid rows (sinks + ring rows filled so far + the real top-K rows;
 // padding rows are never read, Sec. III-B.2).
 //
-//   append        one workgroup per sequence writes k/v of token pos to its row
-//   decode_mfma   per (chunk, sequence, KV head), one wave: bf16 MFMA
-//                 K x q^T for the G heads of the group (padded to 16 columns),
-//                 online softmax in the exp2 domain, MFMA V^T x P^T; bf16 or
-//                 fp8 E4M3 rows (converted to bf16 in registers)
+//   append         one workgroup per sequence writes k/v of token pos to its row
+//   decode_mfma    per (chunk, sequence, KV head), one wave: bf16 MFMA
+//                  K x q^T for the G heads of the group (padded to 16 columns),
+//                  online softmax in the exp2 domain, MFMA V^T x P^T; bf16 or
+//                  fp8 E4M3 rows (converted to bf16 in registers)
+//   decode_mla_lds bf16 latent rows (576 wide, values = first 512 dims): four
+//                  waves per (chunk, sequence) streaming 32-row blocks through
+//                  a 4-stage LDS ring
+//   decode_mla     fp8 latent rows, register-streamed
 //   decode_generic one wave per (chunk, sequence, query head); any dtype
-//   combine       log-sum-exp merge of the chunk partials -> out
+//   combine        log-sum-exp merge of the chunk partials -> out
+// For bf16 caches decode_mfma and decode_mla_lds also take the new token
+// (snap_decode_step): the append happens in the same launch.
 #include <math.h>
 
 #include "snap_internal.h"
