@@ -298,19 +298,23 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
         sl.rz[rb][e] = z;
         sl.rm[rb][e] = mn;
       }
-  } else {
-    lds_barrier();
-    if (tid() < TK) {
-      int j = t0 + tid();
-      const float* c = colbuf + tid();
-      float sum;
-      if constexpr (NW == 4) {
-        sum = (c[0] + c[TK]) + (c[2 * TK] + c[3 * TK]);
-      } else {
-        sum = ((c[0] + c[TK]) + (c[2 * TK] + c[3 * TK])) + ((c[4 * TK] + c[5 * TK]) + (c[6 * TK] + c[7 * TK]));
-      }
-      if (j < c1) a.A[(size_t)bg * a.max_len + j] = sum;
+  }
+}
+
+// Column sums of one tile across the NW waves (fixed order), written to A.
+// The caller places a barrier between the waves' colbuf writes and this.
+template <int NW, int TK>
+__device__ __forceinline__ void colsum_finish(const ScoreArgs& a, const float* colbuf, int t0, int c1, int bg) {
+  if (tid() < TK) {
+    const int j = t0 + tid();
+    const float* c = colbuf + tid();
+    float sum;
+    if constexpr (NW == 4) {
+      sum = (c[0] + c[TK]) + (c[2 * TK] + c[3 * TK]);
+    } else {
+      sum = ((c[0] + c[TK]) + (c[2 * TK] + c[3 * TK])) + ((c[4 * TK] + c[5 * TK]) + (c[6 * TK] + c[7 * TK]));
     }
+    if (j < c1) a.A[(size_t)bg * a.max_len + j] = sum;
   }
 }
 
@@ -328,7 +332,7 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
   constexpr int CPR = kRowBytes / 16;                 // 16-byte chunks per key row
   constexpr int kTileBytes = TK * kRowBytes;
   __shared__ __align__(16) unsigned char tiles[STAGES][kTileBytes];
-  __shared__ float colbuf[NW * TK];
+  __shared__ float colbuf[2][NW * TK];  // column partials, double-buffered for the ring
   __shared__ float qlds[kBF16 ? 1 : 128 * D];           // fp32 inputs: [rows_pad <= 128][D]
 
   const int lane = tid() & 63, wave = tid() >> 6;
@@ -417,8 +421,8 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
   const int nt = (c1 - c0 + TK - 1) / TK;  // tiles of this chunk
   const int nload = tile_loads<CPR, NW, TK>(__builtin_amdgcn_readfirstlane(wave));
   // prologue: tile 0 (the double buffer issues each next tile inside its
-  // loop), or the first STAGES tiles of the ring
-  for (int st = 0; st < (STAGES == 2 ? 1 : STAGES) && st < nt; ++st)
+  // loop), or the first STAGES-1 tiles of the ring
+  for (int st = 0; st < (STAGES == 2 ? 1 : STAGES - 1) && st < nt; ++st)
     issue_tile<CPR, NW, TK>(kbase, kRowBytes, c0 + st * TK, c1, &tiles[st][0], wave, lane);
 
   // a tile is interior when all its keys are in range and precede the first
@@ -444,8 +448,12 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
           wait_vm<0>();
         }
         lds_barrier();  // tile0 holds keys [t0, t0+TK)
-        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile0, qf, qlds, colbuf, sl, t0, c1, interior_of(t0), bg, wave,
-                                               lane, wave_has_rows);
+        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile0, qf, qlds, colbuf[0], sl, t0, c1, interior_of(t0), bg,
+                                               wave, lane, wave_has_rows);
+        if constexpr (COLSUM) {
+          lds_barrier();
+          colsum_finish<NW, TK>(a, colbuf[0], t0, c1, bg);
+        }
       }
       const int t1 = t0 + TK;
       if (t1 < c1) {
@@ -457,20 +465,34 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
           wait_vm<0>();
         }
         lds_barrier();  // tile1 holds keys [t1, t1+TK)
-        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile1, qf, qlds, colbuf, sl, t1, c1, interior_of(t1), bg, wave,
-                                               lane, wave_has_rows);
+        score_tile<In, KSTEPS, NW, COLSUM, TK>(a, tile1, qf, qlds, colbuf[0], sl, t1, c1, interior_of(t1), bg,
+                                               wave, lane, wave_has_rows);
+        if constexpr (COLSUM) {
+          lds_barrier();
+          colsum_finish<NW, TK>(a, colbuf[0], t1, c1, bg);
+        }
       }
     }
   } else {
+    // Ring, one barrier per tile: past the barrier of tile i every wave has
+    // finished tile i-1, so its stage takes tile i+STAGES-1 right away and
+    // its column partials (the other colbuf half) can be summed.
     for (int i = 0; i < nt; ++i) {
-      wait_vm_dyn(min(nt - 1 - i, STAGES - 1) * nload);  // tile i has landed
+      wait_vm_dyn(min(nt - 1 - i, STAGES - 2) * nload);  // tile i has landed
       lds_barrier();                                      // ... for every wave
       const int t = c0 + i * TK;
-      unsigned char* ktile = &tiles[i % STAGES][0];
-      score_tile<In, KSTEPS, NW, COLSUM, TK>(a, ktile, qf, qlds, colbuf, sl, t, c1, interior_of(t), bg, wave,
-                                             lane, wave_has_rows);
-      lds_barrier();  // every wave is done with this stage (and with colbuf)
-      if (i + STAGES < nt) issue_tile<CPR, NW, TK>(kbase, kRowBytes, t + STAGES * TK, c1, ktile, wave, lane);
+      if (i + STAGES - 1 < nt)
+        issue_tile<CPR, NW, TK>(kbase, kRowBytes, t + (STAGES - 1) * TK, c1, &tiles[(i + STAGES - 1) % STAGES][0],
+                                wave, lane);
+      if constexpr (COLSUM) {
+        if (i > 0) colsum_finish<NW, TK>(a, colbuf[(i - 1) & 1], t - TK, c1, bg);
+      }
+      score_tile<In, KSTEPS, NW, COLSUM, TK>(a, &tiles[i % STAGES][0], qf, qlds, colbuf[i & 1], sl, t, c1,
+                                             interior_of(t), bg, wave, lane, wave_has_rows);
+    }
+    if constexpr (COLSUM) {
+      lds_barrier();
+      colsum_finish<NW, TK>(a, colbuf[(nt - 1) & 1], c0 + (nt - 1) * TK, c1, bg);
     }
   }
 
