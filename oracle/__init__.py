@@ -20,7 +20,9 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# SNAP_ORACLE_LIB names another build of oracle.c (the mutation tests load
+# deliberately broken copies this way); by default the in-tree library
+_LIB_PATH = os.environ.get("SNAP_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 POOL_MAX, POOL_AVG = 0, 1
