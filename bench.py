@@ -26,19 +26,42 @@ DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
+def device_code_sha256(lib_path: str):
+    """sha256 of the device code (.hip_fatbin section) of a built library: it
+    changes when any kernel changes and not when only comments do."""
+    import hashlib
+    import struct
+    try:
+        d = open(lib_path, "rb").read()
+    except OSError:
+        return None
+    if d[:5] != b"\x7fELF\x02":
+        return None
+    shoff = struct.unpack_from("<Q", d, 0x28)[0]
+    shentsize, shnum, shstrndx = struct.unpack_from("<HHH", d, 0x3A)
+    sh = lambda i: struct.unpack_from("<IIQQQQ", d, shoff + i * shentsize)  # noqa: E731
+    stroff = sh(shstrndx)[4]
+    for i in range(shnum):
+        name, _, _, _, off, size = sh(i)
+        if d[stroff + name:d.index(b"\0", stroff + name)] == b".hip_fatbin":
+            return hashlib.sha256(d[off:off + size]).hexdigest()
+    return None
+
+
 def measured_traffic(workload: str):
     """HBM bytes per decode-step call from the committed counter runs
-    (profiles/traffic.json), or None when no record exists or the decode
-    kernels have changed since the counters were taken."""
-    import hashlib
+    (profiles/traffic.json), or None when no record exists or the library's
+    device code has changed since the counters were taken."""
     try:
         rec = json.load(open(os.path.join(HERE, "profiles", "traffic.json")))[workload]
-        src = open(os.path.join(HERE, "paper_2511_03092_amd", "csrc", "decode.hip"), "rb").read()
     except (OSError, KeyError, ValueError):
         return None
-    if hashlib.sha256(src).hexdigest() != rec.get("decode_source_sha256"):
+    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"))
+    if code is None or code != rec.get("device_code_sha256"):
         return None
     return rec["traffic_bytes_per_launch"]
+
+
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 
