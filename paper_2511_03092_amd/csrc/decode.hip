@@ -50,7 +50,7 @@ struct DecodeArgs {
 };
 
 struct RowSpan {
-  int n1, v0, v1;
+  int n1, v0, v1, nv;  // first-run length, this chunk's [v0, v1), all valid rows
 };
 
 // Virtual row v in [0, n1 + n_topk) -> cache row: the first n1 are sinks and
@@ -73,6 +73,7 @@ __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, i
   int cs = (nv + a.n_chunks - 1) / a.n_chunks;
   cs = (cs + 31) & ~31;
   sp.n1 = n1;
+  sp.nv = nv;
   sp.v0 = chunk * cs;
   sp.v1 = min(sp.v0 + cs, nv);
   return true;
@@ -608,13 +609,20 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   const unsigned char* knew = vnew >= 0 ? (const unsigned char*)a.k_new + (size_t)b * kLatRowBytes : nullptr;
   u32x4 newp = {0u, 0u, 0u, 0u};
   const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, 0, tid(), newp);
-  const int nblk = __builtin_amdgcn_readfirstlane((sp.v1 - sp.v0 + 31) / 32);
+  // The slot's 32-row blocks are interleaved over its chunks: block i of
+  // this chunk is the slot's block chunk + i * n_chunks.  At any moment the
+  // chunks of a slot read one window of neighbouring blocks, which spreads
+  // the requests over the memory channels (measured 1% faster than
+  // contiguous chunk ranges).
+  const int nb_slot = (sp.nv + 31) / 32;
+  const int nblk =
+      __builtin_amdgcn_readfirstlane(chunk < nb_slot ? (nb_slot - chunk + a.n_chunks - 1) / a.n_chunks : 0);
   auto issue = [&](int blk) {
-    const int vb = sp.v0 + 32 * blk;
+    const int vb = 32 * (chunk + blk * a.n_chunks);
     unsigned char* dst = &stage[blk % kLatStages][0];
     // a whole block inside one run of the row map, without the new token:
     // 32 consecutive cache rows from a uniform base
-    const bool plain = vb + 32 <= sp.v1 && (vb + 32 <= sp.n1 || vb >= sp.n1) && !(vnew >= vb && vnew < vb + 32);
+    const bool plain = vb + 32 <= sp.nv && (vb + 32 <= sp.n1 || vb >= sp.n1) && !(vnew >= vb && vnew < vb + 32);
     if (plain) {
       const unsigned char* base = cache + (size_t)virt_row(vb, sp.n1, sr) * kLatRowBytes;
 #pragma unroll
@@ -623,7 +631,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
 #pragma unroll
       for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
         int v = vb + ld_r[ii];
-        v = v < sp.v1 ? v : sp.v1 - 1;
+        v = v < sp.nv ? v : sp.nv - 1;
         const unsigned char* src =
             (v == vnew ? knew : cache + (size_t)virt_row(v, sp.n1, sr) * kLatRowBytes) + ld_c[ii] * 16;
         dma16_lat(src, dst + (size_t)(wu + 4 * ii) * 1024);
@@ -683,7 +691,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
       lat_wait_vm<0>();
     lat_barrier();  // block i is in LDS for every wave
     const unsigned char* st = &stage[i % kLatStages][0];
-    const int vb = sp.v0 + 32 * i;
+    const int vb = 32 * (chunk + i * a.n_chunks);
 
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -705,7 +713,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     // raw dot products; the scale (> 0) is applied to the block max and folded
     // into the exponent
     float x[8];
-    if (vb + 32 <= sp.v1) {
+    if (vb + 32 <= sp.nv) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         x[e] = s0[e];
@@ -714,8 +722,8 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        x[e] = (vb + 4 * lg + e < sp.v1) ? s0[e] : -INFINITY;
-        x[4 + e] = (vb + 16 + 4 * lg + e < sp.v1) ? s1[e] : -INFINITY;
+        x[e] = (vb + 4 * lg + e < sp.nv) ? s0[e] : -INFINITY;
+        x[4 + e] = (vb + 16 + 4 * lg + e < sp.nv) ? s1[e] : -INFINITY;
       }
     }
     float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
