@@ -129,3 +129,34 @@ def test_decode_and_append_validation():
     assert st == snap.SNAP_ERR_INVALID_ARG  # v_new missing
     assert L.snap_advance(FAKE, 0, 1, FAKE, None) == snap.SNAP_ERR_INVALID_ARG
     assert L.snap_advance(FAKE, 4, 0, FAKE, None) == snap.SNAP_OK
+
+
+def test_decode_step_validation():
+    """snap_decode_step checks everything snap_cache_append and
+    snap_decode_attn check, before any launch."""
+    L = snap.lib()
+    p = _params()
+    cache = snap.SnapCache(FAKE, FAKE, None, None, 4)
+    big = 1 << 30
+
+    def step(q=FAKE, k_new=FAKE, v_new=FAKE, out=FAKE, out_dtype=snap.SNAP_BF16, ws=FAKE, ws_bytes=big, n=2,
+             params=p, c=cache):
+        return L.snap_decode_step(ctypes.byref(params.c()), ctypes.byref(c), FAKE, FAKE, n, FAKE, q, k_new, v_new,
+                                  out, out_dtype, ws, ws_bytes, None)
+
+    assert step(k_new=None) == snap.SNAP_ERR_INVALID_ARG
+    assert step(k_new=FAKE + 4) == snap.SNAP_ERR_INVALID_ARG           # misaligned
+    assert step(v_new=None) == snap.SNAP_ERR_INVALID_ARG               # GQA cache needs v_new
+    assert step(q=None) == snap.SNAP_ERR_INVALID_ARG
+    assert step(out=FAKE + 8) == snap.SNAP_ERR_INVALID_ARG
+    assert step(out_dtype=snap.SNAP_FP8_E4M3) == snap.SNAP_ERR_INVALID_ARG
+    assert step(ws_bytes=16) == snap.SNAP_ERR_WORKSPACE
+    assert step(ws=FAKE + 64) == snap.SNAP_ERR_WORKSPACE               # not 256-byte aligned
+    assert step(n=-1) == snap.SNAP_ERR_INVALID_ARG
+    assert step(n=0) == snap.SNAP_OK                                   # no-op
+    assert step(params=_params(pool_kernel=4)) == snap.SNAP_ERR_INVALID_ARG
+    # latent cache: values live in K, so v_new must be absent
+    lat = _params(n_q_heads=8, n_kv_heads=1, d_qk=576, d_v=512, v_in_k=1, recent=4096, topk=28668)
+    lcache = snap.SnapCache(FAKE, None, None, None, 4)
+    assert step(params=lat, c=lcache, ws_bytes=16) == snap.SNAP_ERR_WORKSPACE   # v_new ignored, then ws
+    assert b"workspace" in snap.lib().snap_last_error()
