@@ -26,9 +26,11 @@ DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def device_code_sha256(lib_path: str):
-    """sha256 of the device code (.hip_fatbin section) of a built library: it
-    changes when any kernel changes and not when only comments do."""
+def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
+    """sha256 of the gfx950 code object, in a built library's .hip_fatbin
+    section, that defines `symbol` (by default the decode kernels' object,
+    which also holds the combine): it changes when one of that object's kernels
+    changes, and not when only comments or the other objects' kernels do."""
     import hashlib
     import struct
     try:
@@ -41,17 +43,35 @@ def device_code_sha256(lib_path: str):
     shentsize, shnum, shstrndx = struct.unpack_from("<HHH", d, 0x3A)
     sh = lambda i: struct.unpack_from("<IIQQQQ", d, shoff + i * shentsize)  # noqa: E731
     stroff = sh(shstrndx)[4]
+    fat = None
     for i in range(shnum):
         name, _, _, _, off, size = sh(i)
         if d[stroff + name:d.index(b"\0", stroff + name)] == b".hip_fatbin":
-            return hashlib.sha256(d[off:off + size]).hexdigest()
+            fat = d[off:off + size]
+    if fat is None:
+        return None
+    # offload bundles: magic, entry count, then (offset, size, triple length,
+    # triple) per entry, offsets from the bundle's start
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    b = fat.find(magic)
+    while b >= 0:
+        n = struct.unpack_from("<Q", fat, b + len(magic))[0]
+        o = b + len(magic) + 8
+        for _ in range(n):
+            off, size, tl = struct.unpack_from("<QQQ", fat, o)
+            triple = fat[o + 24:o + 24 + tl]
+            o += 24 + tl
+            code = fat[b + off:b + off + size]
+            if triple.endswith(b"gfx950") and symbol in code:
+                return hashlib.sha256(code).hexdigest()
+        b = fat.find(magic, b + 1)
     return None
 
 
 def measured_traffic(workload: str):
     """HBM bytes per decode-step call from the committed counter runs
-    (profiles/traffic.json), or None when no record exists or the library's
-    device code has changed since the counters were taken."""
+    (profiles/traffic.json), or None when no record exists or the decode
+    kernels' code object has changed since the counters were taken."""
     try:
         rec = json.load(open(os.path.join(HERE, "profiles", "traffic.json")))[workload]
     except (OSError, KeyError, ValueError):
