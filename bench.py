@@ -89,14 +89,18 @@ PEAK_BF16_TFLOPS = 2500.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 3; 64 for the continuous-batching workload)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps first (default 1; 32 for the continuous-batching workload)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--two-calls", action="store_true",
                     help="decode with snap_cache_append + snap_decode_attn instead of snap_decode_step")
+    ap.add_argument("--graph", action="store_true",
+                    help="run each step's decode phase as one captured HIP graph (replayed every step)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
     return ap.parse_args()
@@ -116,9 +120,11 @@ def main():
 
     wl = synth.WORKLOADS[args.workload]
     if wl.slots is not None:
-        print("the continuous-batching workload is benchmarked by its own driver loop (not yet wired here)",
-              file=sys.stderr)
-        sys.exit(2)
+        return run_cb(args, wl)
+    if args.steps is None:
+        args.steps = 3
+    if args.warmup is None:
+        args.warmup = 1
     layers = args.layers or wl.layers
     dsteps = wl.decode_steps if args.decode_steps is None else args.decode_steps
     dev = torch.device("cuda:0")
@@ -170,6 +176,21 @@ def main():
         e.record(stream)
         return e
 
+    def decode_phase(sp):
+        for t in range(dsteps):
+            for l in range(layers):
+                qd, kd, vd = dec[l]
+                if args.two_calls:
+                    snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t],
+                                           stream=sp)
+                    snap.snap_decode_attn(p, caches[l][2], pos, ntop, slots, qd[t], out, wsd, stream=sp)
+                else:
+                    snap.snap_decode_step(p, caches[l][2], pos, ntop, slots, qd[t], kd[t],
+                                          None if vd is None else vd[t], out, wsd, stream=sp)
+            snap.snap_advance(pos, slots, stream=sp)
+
+    graph = []
+
     def step(timing):
         if timing is not None:
             c0 = ev()
@@ -178,23 +199,25 @@ def main():
             snap.snap_compress(p, caches[l][2], pos, ntop, slots, lens, q, k, v, wsc, stream=sptr)
         if timing is not None:
             timing["compress"].append((c0, ev()))
-        for t in range(dsteps):
-            for l in range(layers):
-                qd, kd, vd = dec[l]
-                if args.two_calls:
-                    snap.snap_cache_append(p, caches[l][2], pos, slots, kd[t], None if vd is None else vd[t],
-                                           stream=sptr)
-                    snap.snap_decode_attn(p, caches[l][2], pos, ntop, slots, qd[t], out, wsd, stream=sptr)
-                else:
-                    snap.snap_decode_step(p, caches[l][2], pos, ntop, slots, qd[t], kd[t],
-                                          None if vd is None else vd[t], out, wsd, stream=sptr)
-            snap.snap_advance(pos, slots, stream=sptr)
+        if graph:
+            graph[0].replay()
+        else:
+            decode_phase(sptr)
         if timing is not None:
             timing["decode"].append((timing["compress"][-1][1], ev()))
 
     for _ in range(args.warmup):
         step(None)
     torch.cuda.synchronize()
+    if args.graph:
+        # the whole decode phase of a step (every layer's decode calls and the
+        # advances) captured once; every timed step compresses eagerly, then
+        # replays it on the same stream
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            decode_phase(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        graph.append(g)
     timing = {"compress": [], "decode": []}
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -254,6 +277,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if wl.in_dtype == "bf16" else "f32",
         "data": "synthetic",
+        "launch": "hip_graph" if args.graph else "eager",
         "config": {"workload": wl.name, "layers": layers, "sequences": n, "prompt_lengths": lengths,
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "decode_steps": dsteps,
@@ -276,17 +300,191 @@ def main():
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl, p, lengths, layers, dsteps, n, value)
+        res["cpu_baseline"] = cpu_baseline(wl, p, lengths, n, layers, dsteps, n * dsteps, value)
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value, comp_budget_s=10.0, dec_budget_s=2.0):
+def run_cb(args, wl):
+    """Continuous batching over wl.slots static cache slots (every layer has
+    its own caches; slot metadata is shared).  All slots are filled first
+    (untimed).  Step t then retires slot t mod slots: snap_compress of a new
+    prompt into it for every layer, then one decode step (snap_decode_step per
+    layer, snap_advance) over the other slots.  Prompts are prefixes, of a
+    seeded length in the workload's range, of one 128k-token K/V bank per
+    layer resident in HBM, each with its own observation-window queries.  fp8
+    cache scales are per (slot, KV head) amax / 448, set by this harness: the
+    amax is taken over the layer's whole bank (an upper bound for every
+    prefix), once, before the timed region."""
+    import torch
+
+    import paper_2511_03092_amd as snap
+    import synth
+
+    if args.steps is None:
+        args.steps = 64
+    if args.warmup is None:
+        args.warmup = wl.slots
+    S = wl.slots
+    layers = args.layers or wl.layers
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
+    p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
+                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype])
+    B = p.budget
+    Lmax = wl.max_len
+    n_steps = args.warmup + args.steps
+    nd = S - 1  # sequences decoded per step
+    lengths = synth.draw_lengths(wl, 0, S + n_steps)  # the initial fill, then one prompt per step
+    kvt = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}[wl.kv_dtype]
+
+    t_setup = time.time()
+    banks, caches, obsq, dec = [], [], [], []
+    for l in range(layers):
+        _, kb, vb = synth.prefill(wl, l, 0, Lmax, device=dev)
+        kb, vb = kb.unsqueeze(0), vb.unsqueeze(0)  # [1][Hkv][Lmax][d]
+        banks.append((kb, vb))
+        ck = torch.zeros((S, wl.n_kv_heads, B, wl.d_qk), dtype=kvt, device=dev)
+        cv = torch.zeros((S, wl.n_kv_heads, B, wl.d_v), dtype=kvt, device=dev)
+        ks = (kb[0].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0).repeat(S, 1).contiguous()
+        vs = (vb[0].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0).repeat(S, 1).contiguous()
+        caches.append((ck, cv, ks, vs, snap.cache_struct(ck, cv, ks, vs)))
+        # observation-window queries of every prompt (initial fill, then one per step)
+        obsq.append(torch.stack([synth.obs_queries(wl, l, 1000 + i, lengths[i], device=dev)
+                                 for i in range(S + n_steps)]).contiguous())
+        dec.append(synth.decode_inputs_all(wl, l, n_steps, lengths[1:S], device=dev))
+    pos = torch.full((S,), -1, dtype=torch.int32, device=dev)
+    ntop = torch.zeros((S,), dtype=torch.int32, device=dev)
+    slot_ids = torch.arange(S, dtype=torch.int32, device=dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    # the decoded slots of the step that retires slot r: every slot but r
+    live = [torch.tensor([x for x in range(S) if x != r], dtype=torch.int32, device=dev) for r in range(S)]
+    wsc = snap.workspace(snap.snap_compress_workspace(p, 1, Lmax), dev)
+    wsd = snap.workspace(snap.snap_decode_workspace(p, nd), dev)
+    out = torch.empty((nd, wl.n_q_heads, wl.d_v), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+
+    def compress(i, slot):
+        for l in range(layers):
+            kb, vb = banks[l]
+            snap.snap_compress(p, caches[l][4], pos, ntop, slot_ids[slot:slot + 1], lens[i:i + 1],
+                               obsq[l][i:i + 1], kb, vb, wsc, stream=sptr)
+
+    def decode(t, retired):
+        for l in range(layers):
+            qd, kd, vd = dec[l]
+            snap.snap_decode_step(p, caches[l][4], pos, ntop, live[retired], qd[t], kd[t], vd[t], out, wsd,
+                                  stream=sptr)
+        snap.snap_advance(pos, live[retired], stream=sptr)
+
+    for r in range(S):  # fill every slot
+        compress(r, r)
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    # host mirror of each slot's prompt length and position, for the bytes count
+    slot_len = list(lengths[:S])
+    slot_pos = list(lengths[:S])
+    s_r, row_bytes = wl.sink + wl.recent, (wl.d_qk + wl.d_v) * (1 if wl.kv_dtype == "fp8" else 2)
+    timing = {"compress": [], "decode": []}
+    dec_bytes, timed_lengths = 0, []
+    t0 = t1 = None
+    for t in range(n_steps):
+        timed = t >= args.warmup
+        if t == args.warmup:
+            torch.cuda.synchronize()
+            t0 = ev()
+        r = t % S
+        i = S + t
+        c0 = ev() if timed else None
+        compress(i, r)
+        c1 = ev() if timed else None
+        decode(t, r)
+        if timed:
+            timing["compress"].append((c0, c1))
+            timing["decode"].append((c1, ev()))
+            timed_lengths.append(lengths[i])
+        slot_len[r] = slot_pos[r] = lengths[i]
+        for x in range(S):
+            if x == r:
+                continue
+            if timed:
+                ncand = max(slot_len[x] - s_r, 0)
+                dec_bytes += layers * (wl.n_kv_heads * (min(slot_pos[x] + 1, s_r) + min(ncand, wl.topk)) * row_bytes
+                                       + wl.n_kv_heads * 2 * 4)  # rows + the two scales
+            slot_pos[x] += 1
+    t1 = ev()
+    torch.cuda.synchronize()
+    K = args.steps
+    ms_step = t0.elapsed_time(t1) / K
+    comp_ms = sum(a.elapsed_time(b) for a, b in timing["compress"]) / (K * layers)
+    dec_ms = sum(a.elapsed_time(b) for a, b in timing["decode"]) / (K * layers)
+    # per decode call: q and out (bf16), the new token read (bf16) and written (fp8)
+    io = nd * (wl.n_q_heads * (wl.d_qk + wl.d_v) * 2 + wl.n_kv_heads * (wl.d_qk + wl.d_v) * (2 + 1))
+    dec_bytes_call = dec_bytes / (K * layers) + io
+    dec_gbps = dec_bytes_call / (dec_ms * 1e-3) / 1e9
+    G = wl.n_q_heads // wl.n_kv_heads
+    score_flop = sum(wl.n_kv_heads * 2 * G * min(wl.obs_window, L) * wl.d_qk * max(L - s_r, 0)
+                     for L in timed_lengths) / K
+    score_tflops = 2 * score_flop / (comp_ms * 1e-3) / 1e12 if comp_ms > 0 else 0.0
+    value = nd * K / (t0.elapsed_time(t1) * 1e-3)
+    res = {
+        "metric": "compressed-KV decode tok/s/GPU + HBM GB/s at 128k; snap_compress latency",
+        "value": round(value, 2),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "launch": "eager",
+        "config": {"workload": wl.name, "layers": layers, "slots": S, "decoded_per_step": nd,
+                   "prompt_length_range": list(wl.length_range), "prompt_bank_tokens": Lmax,
+                   "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
+                   "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "q_heads": wl.n_q_heads,
+                   "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v, "kv_dtype": wl.kv_dtype,
+                   "step": "compress one new prompt into the retired slot (every layer), then one decode "
+                           "step of the other slots"},
+        "decode_step_ms_per_call": round(dec_ms, 4),
+        "decode_step_hbm_gbps": round(dec_gbps, 1),
+        "decode_only_tok_s": round(nd / (dec_ms * layers * 1e-3), 1) if dec_ms > 0 else 0.0,
+        "compress_ms_per_layer_call": round(comp_ms, 4),
+        "compress_ms_per_seq_layer": round(comp_ms, 4),
+        "score_gemm": {"gflop_per_layer_call_one_pass": round(score_flop / 1e9, 2), "passes": 2,
+                       "tflops_over_compress_call": round(score_tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
+                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4)},
+        "roofline": {"bound": "hbm",
+                     "kernel": "snap_decode_step (fp8 cache: append + split-K attention) + combine",
+                     "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(wl.name),
+                     "algorithmic_bytes_per_launch": round(dec_bytes_call)},
+        "setup_s": round(t_setup, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, p, timed_lengths, nd, layers, K, nd * K, value)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_value, comp_budget_s=10.0,
+                 dec_budget_s=2.0):
     """The fp64 oracle, single-threaded on the host, on a bounded sample of the
     same workload: compress units (one sequence x one KV head) at the longest
     prompt, cycling over the KV heads, until about comp_budget_s of work, and
     decode units (one sequence x one KV head x one step) over the cache that
-    built, until about dec_budget_s; extrapolated to a whole step by unit
-    counts (compress scaled by each sequence's length)."""
+    built, until about dec_budget_s; extrapolated by unit counts to the timed
+    work: every prompt in comp_lengths compressed (scaled by its length) and
+    dsteps decode steps of dec_seqs sequences, every layer, for `tokens`
+    decoded tokens."""
     import numpy as np
 
     import oracle
@@ -294,7 +492,7 @@ def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value, comp_budget_s=10.
 
     op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
                        p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
-    L = max(lengths)
+    L = max(comp_lengths)
     q, k, v = synth.prefill(wl, 0, 0, L, device="cpu")
     G = op.group
     n_comp, t_all, res = 0, 0.0, None
@@ -316,15 +514,16 @@ def cpu_baseline(wl, p, lengths, layers, dsteps, n, gpu_value, comp_budget_s=10.
         t_all += time.time() - t
         n_dec += 1
     t_dec = t_all / n_dec
-    units_comp = layers * n * p.n_kv_heads
-    comp_s = sum(t_comp * (Lb / L) for Lb in lengths) * layers * p.n_kv_heads
-    dec_s = t_dec * layers * n * p.n_kv_heads * dsteps
-    val = n * dsteps / (comp_s + dec_s)
+    units_comp = layers * len(comp_lengths) * p.n_kv_heads
+    units_dec = layers * dec_seqs * p.n_kv_heads * dsteps
+    comp_s = sum(t_comp * (Lb / L) for Lb in comp_lengths) * layers * p.n_kv_heads
+    dec_s = t_dec * units_dec
+    val = tokens / (comp_s + dec_s)
     return {"value": float(f"{val:.6g}"), "unit": "tok/s", "cores": 1, "kind": "oracle",
             "sample": (f"{n_comp} compress units (1 sequence x 1 KV head, L={L}) at {t_comp:.2f} s each and "
                        f"{n_dec} decode units (1 sequence x 1 KV head x 1 step) at {t_dec * 1e3:.1f} ms each, "
                        f"single thread; extrapolated to {units_comp} compress units (scaled by length) and "
-                       f"{layers * n * p.n_kv_heads * dsteps} decode units per step"),
+                       f"{units_dec} decode units for {tokens} tokens"),
             "gpu_over_cpu": float(f"{gpu_value / val:.4g}")}
 
 

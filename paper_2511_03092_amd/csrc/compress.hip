@@ -172,133 +172,165 @@ __device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c
   return fast_exp2(yh - c) * fmaf(yl, invl, inv);
 }
 
-// One 64-key tile already resident in LDS: scores for this wave's 32 rows,
-// then either the running row max / sum of powers of two (STATS) or the
+// Scores of one TK-key tile already resident in LDS against this wave's 32
+// rows, then either the running row max / sum of powers of two (STATS) or the
 // column sums of the normalised weights written to A (COLSUM).  Logits are
 // kept in log2 units, y = <q,k> * scale * log2(e), formed by one rounded
 // multiply, so exp(z) = exp2(y).  `interior` (uniform) means every key of the
 // tile is a candidate that precedes every window row: no per-element masks.
+// The work is split per 16-key sub-block into the products (score_mma_sb) and
+// the softmax arithmetic (score_epi_sb), so a caller can run the two halves of
+// a tile at different times.
+//
 // LDS fragment reads issued ahead of their MFMAs (measured: 4 is 4% faster
 // than the scheduler's own 2 on the latent shape; 6 is no better).
 constexpr int kReadAhead = 4;
+
+// Products of sub-block sb (keys sb*16 .. sb*16+15 of the tile): acc[rb] holds
+// rows rb*16 + 4*(lane/16) + e (e = 0..3) against key sb*16 + lane%16.
+template <typename In, int KSTEPS, int TK>
+__device__ __forceinline__ void score_mma_sb(const unsigned char* __restrict__ ktile, const bf16x8 (&qf)[2][KSTEPS],
+                                             const float* qlds, int sb, int wave, int lane, bool wave_has_rows,
+                                             f32x4 (&acc)[2]) {
+  constexpr bool kBF16 = sizeof(In) == 2;
+  constexpr int D = KSTEPS * 32;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int key = sb * 16 + l16;
+  acc[0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  acc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (kBF16) {
+    // waves without score rows multiply zero fragments (only tiny cases have them).
+    // Even and odd k-steps accumulate in separate chains (shorter fp32
+    // accumulation, two independent MFMA chains), summed at the end.
+    f32x4 odd[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot<TK>(key, KSTEPS * lg + t) * 16));
+      if (t & 1) {
+        odd[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, odd[0], 0, 0, 0);
+        odd[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, odd[1], 0, 0, 0);
+      } else {
+        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
+      }
+    }
+    // the fragment reads run kReadAhead k-steps ahead of the MFMAs that use
+    // them, so their LDS latency hides behind earlier products
+    __builtin_amdgcn_sched_group_barrier(0x100, kReadAhead, 0);  // DS reads
+#pragma unroll
+    for (int t = 0; t < KSTEPS - kReadAhead; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * kReadAhead, 0);
+    acc[0] += odd[0];
+    acc[1] += odd[1];
+  } else if (wave_has_rows) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
+        // fp32 products are exact in fp64; only the final rounding remains
+        double sacc = 0.0;
+#pragma unroll 4
+        for (int d = 0; d < D; ++d) {
+          const float kd = *(const float*)(ktile + (size_t)tile_slot<TK>(key, d >> 2) * 16 + (d & 3) * 4);
+          sacc = fma((double)qrow[d], (double)kd, sacc);
+        }
+        acc[rb][e] = (float)sacc;
+      }
+  }
+}
+
+// Softmax arithmetic of sub-block sb from its products: STATS keeps the scaled
+// logits in xv for score_stats_tile; COLSUM writes this wave's column sums of
+// the normalised weights to colbuf.
+template <int NW, bool COLSUM, int TK>
+__device__ __forceinline__ void score_epi_sb(const ScoreArgs& a, const f32x4 (&acc)[2], float* colbuf,
+                                             const ScoreLane& sl, int t0, int c1, bool interior, int sb, int wave,
+                                             int lane, float (&xv)[2][4][TK / 16]) {
+  const int l16 = lane & 15, lg = lane >> 4;
+  const float s2 = a.scale2, s2lo = a.scale2_lo;
+  const int key = sb * 16 + l16;
+  const int j = t0 + key;
+  if (!COLSUM) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) xv[rb][e][sb] = acc[rb][e] * s2;
+    if (!interior) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) xv[rb][e][sb] = -INFINITY;
+    }
+  } else {
+    float colv[2][4];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        colv[rb][e] = weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]);
+    if (!interior) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) colv[rb][e] = 0.f;
+    }
+    float cs = ((colv[0][0] + colv[0][1]) + (colv[0][2] + colv[0][3])) +
+               ((colv[1][0] + colv[1][1]) + (colv[1][2] + colv[1][3]));
+    cs += __shfl_xor(cs, 16);
+    cs += __shfl_xor(cs, 32);
+    if (lg == 0) colbuf[wave * TK + sb * 16 + l16] = cs;
+  }
+}
+
+// STATS: fold one tile's scaled logits into the running row max / sum.
+template <int TK>
+__device__ __forceinline__ void score_stats_tile(ScoreLane& sl, const float (&xv)[2][4][TK / 16]) {
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float* x = xv[rb][e];
+      float mt, mn;
+      if constexpr (TK == 64) {
+        mt = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      } else {
+        mt = fmaxf(x[0], x[1]);
+      }
+      mn = fmaxf(sl.rm[rb][e], mt);
+      if (mn == -INFINITY) continue;
+      float z = sl.rz[rb][e] * fast_exp2(sl.rm[rb][e] - mn);
+      if constexpr (TK == 64) {
+        z += (fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) + (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn));
+      } else {
+        z += fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn);
+      }
+      sl.rz[rb][e] = z;
+      sl.rm[rb][e] = mn;
+    }
+}
+
+// The whole tile in one go: products and softmax arithmetic sub-block by
+// sub-block.
 template <typename In, int KSTEPS, int NW, bool COLSUM, int TK>
 __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned char* __restrict__ ktile,
                                            const bf16x8 (&qf)[2][KSTEPS], const float* qlds, float* colbuf,
                                            ScoreLane& sl, int t0, int c1, bool interior, int bg, int wave,
                                            int lane, bool wave_has_rows) {
-  constexpr bool kBF16 = sizeof(In) == 2;
-  constexpr int D = KSTEPS * 32;
   static_assert(TK == 64 || TK == 32, "tile of 64 or 32 keys");
-  const int l16 = lane & 15, lg = lane >> 4;
-  const float s2 = a.scale2, s2lo = a.scale2_lo;
   float xv[2][4][TK / 16];
 #pragma unroll
   for (int sb = 0; sb < TK / 16; ++sb) {
-    f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    const int key = sb * 16 + l16;
-    if constexpr (kBF16) {
-      // waves without score rows multiply zero fragments (only tiny cases have them).
-      // Even and odd k-steps accumulate in separate chains (shorter fp32
-      // accumulation, two independent MFMA chains), summed at the end.
-      f32x4 odd[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-      for (int t = 0; t < KSTEPS; ++t) {
-        bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(ktile + (size_t)tile_slot<TK>(key, KSTEPS * lg + t) * 16));
-        if (t & 1) {
-          odd[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, odd[0], 0, 0, 0);
-          odd[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, odd[1], 0, 0, 0);
-        } else {
-          acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[0][t], kf, acc[0], 0, 0, 0);
-          acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[1][t], kf, acc[1], 0, 0, 0);
-        }
-      }
-      // the fragment reads run kReadAhead k-steps ahead of the MFMAs that use
-      // them, so their LDS latency hides behind earlier products
-      __builtin_amdgcn_sched_group_barrier(0x100, kReadAhead, 0);  // DS reads
-#pragma unroll
-      for (int t = 0; t < KSTEPS - kReadAhead; ++t) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 2 * kReadAhead, 0);
-      acc[0] += odd[0];
-      acc[1] += odd[1];
-    } else if (wave_has_rows) {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float* qrow = qlds + (size_t)(wave * 32 + rb * 16 + lg * 4 + e) * D;
-          // fp32 products are exact in fp64; only the final rounding remains
-          double sacc = 0.0;
-#pragma unroll 4
-          for (int d = 0; d < D; ++d) {
-            const float kd = *(const float*)(ktile + (size_t)tile_slot<TK>(key, d >> 2) * 16 + (d & 3) * 4);
-            sacc = fma((double)qrow[d], (double)kd, sacc);
-          }
-          acc[rb][e] = (float)sacc;
-        }
-    }
-    const int j = t0 + key;
-    float colv[2][4];
-    if (!COLSUM) {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) xv[rb][e][sb] = acc[rb][e] * s2;
-      if (!interior) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) xv[rb][e][sb] = -INFINITY;
-      }
-    } else {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          colv[rb][e] = weight(acc[rb][e], s2, s2lo, sl.rc[rb][e], sl.rinv[rb][e], sl.rinvl[rb][e]);
-      if (!interior) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (!(sl.rval[rb][e] && j < c1 && j <= sl.rpos[rb][e])) colv[rb][e] = 0.f;
-      }
-    }
-    if (COLSUM) {
-      float cs = ((colv[0][0] + colv[0][1]) + (colv[0][2] + colv[0][3])) +
-                 ((colv[1][0] + colv[1][1]) + (colv[1][2] + colv[1][3]));
-      cs += __shfl_xor(cs, 16);
-      cs += __shfl_xor(cs, 32);
-      if (lg == 0) colbuf[wave * TK + sb * 16 + l16] = cs;
-    }
+    f32x4 acc[2];
+    score_mma_sb<In, KSTEPS, TK>(ktile, qf, qlds, sb, wave, lane, wave_has_rows, acc);
+    score_epi_sb<NW, COLSUM, TK>(a, acc, colbuf, sl, t0, c1, interior, sb, wave, lane, xv);
   }
-  if (!COLSUM) {
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float* x = xv[rb][e];
-        float mt, mn;
-        if constexpr (TK == 64) {
-          mt = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-        } else {
-          mt = fmaxf(x[0], x[1]);
-        }
-        mn = fmaxf(sl.rm[rb][e], mt);
-        if (mn == -INFINITY) continue;
-        float z = sl.rz[rb][e] * fast_exp2(sl.rm[rb][e] - mn);
-        if constexpr (TK == 64) {
-          z += (fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) + (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn));
-        } else {
-          z += fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn);
-        }
-        sl.rz[rb][e] = z;
-        sl.rm[rb][e] = mn;
-      }
-  }
+  if (!COLSUM) score_stats_tile<TK>(sl, xv);
 }
 
 // Column sums of one tile across the NW waves (fixed order), written to A.
@@ -470,6 +502,60 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
         if constexpr (COLSUM) {
           lds_barrier();
           colsum_finish<NW, TK>(a, colbuf[0], t1, c1, bg);
+        }
+      }
+    }
+  } else if constexpr (kBF16 && NW == 8) {
+    // Ring in ping-pong: waves 0-3 (group A) and 4-7 (group B; each SIMD
+    // holds one wave of each) run half a tile apart, two barriers per tile.
+    // In the first half of step i group A multiplies tile i while group B runs
+    // the softmax arithmetic of tile i-1; in the second half A runs tile i's
+    // arithmetic while B multiplies tile i.  So matrix and vector work of the
+    // two waves of a SIMD overlap instead of taking turns.  Past the first
+    // barrier of step i every wave is done reading tile i-1, so its stage
+    // takes tile i+STAGES-1; past the second, both groups' column partials of
+    // tile i-1 are in colbuf.
+    const bool grp_a = __builtin_amdgcn_readfirstlane(wave) < NW / 2;
+    f32x4 acc[TK / 16][2];
+    int tp = c0;  // first key of the tile this wave multiplied last
+    for (int i = 0; i <= nt; ++i) {
+      const int t = c0 + i * TK;
+      if (i < nt) wait_vm_dyn(min(nt - 1 - i, STAGES - 2) * nload);  // tile i has landed
+      lds_barrier();                                                 // ... for every wave
+      if (i + STAGES - 1 < nt)
+        issue_tile<CPR, NW, TK>(kbase, kRowBytes, t + (STAGES - 1) * TK, c1, &tiles[(i + STAGES - 1) % STAGES][0],
+                                wave, lane);
+      if (grp_a ? i < nt : i > 0) {
+        if (grp_a) {
+#pragma unroll
+          for (int sb = 0; sb < TK / 16; ++sb)
+            score_mma_sb<In, KSTEPS, TK>(&tiles[i % STAGES][0], qf, qlds, sb, wave, lane, wave_has_rows, acc[sb]);
+          tp = t;
+        } else {
+          float xv[2][4][TK / 16];
+#pragma unroll
+          for (int sb = 0; sb < TK / 16; ++sb)
+            score_epi_sb<NW, COLSUM, TK>(a, acc[sb], colbuf[(i - 1) & 1], sl, tp, c1, interior_of(tp), sb, wave,
+                                         lane, xv);
+          if (!COLSUM) score_stats_tile<TK>(sl, xv);
+        }
+      }
+      lds_barrier();
+      if constexpr (COLSUM) {
+        if (i > 0) colsum_finish<NW, TK>(a, colbuf[(i - 1) & 1], t - TK, c1, bg);
+      }
+      if (i < nt) {
+        if (grp_a) {
+          float xv[2][4][TK / 16];
+#pragma unroll
+          for (int sb = 0; sb < TK / 16; ++sb)
+            score_epi_sb<NW, COLSUM, TK>(a, acc[sb], colbuf[i & 1], sl, tp, c1, interior_of(tp), sb, wave, lane, xv);
+          if (!COLSUM) score_stats_tile<TK>(sl, xv);
+        } else {
+#pragma unroll
+          for (int sb = 0; sb < TK / 16; ++sb)
+            score_mma_sb<In, KSTEPS, TK>(&tiles[i % STAGES][0], qf, qlds, sb, wave, lane, wave_has_rows, acc[sb]);
+          tp = t;
         }
       }
     }

@@ -169,6 +169,16 @@ def plant_direction(wl: Workload, layer: int, kv_head: int) -> torch.Tensor:
     return (u / u.norm()).to(torch.float32)
 
 
+def obs_queries(wl: Workload, layer: int, slot: int, L: int, device="cpu", salt: int = 0) -> torch.Tensor:
+    """The observation-window queries of one prompt alone, q_obs [Hq][w][dqk]:
+    the same tensor prefill() returns for these arguments."""
+    w = wl.obs_window
+    q = _randn((wl.n_q_heads, w, wl.d_qk), seed_of(wl.cfg_id, layer, slot, P_Q, salt), device)
+    if wl.rope:
+        rope_(q, torch.arange(L - w, L, device=device), wl.rope_theta)
+    return cast(q, wl.in_dtype)
+
+
 def prefill(wl: Workload, layer: int, slot: int, L: int, device="cpu", salt: int = 0,
             max_len: int | None = None, pad_value: float = 0.0):
     """Inputs of one sequence: q_obs [Hq][w][dqk], k [Hkv][Lpad][k_width], v [Hkv][Lpad][dv]
