@@ -175,11 +175,12 @@ snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, cons
 
 /* One layer's decode step (Sec. III-C): snap_cache_append(k_new, v_new)
  * followed by snap_decode_attn, with the same arguments, results and cache
- * contents as those two calls on the same stream.  For bf16 caches of the
- * supported MFMA shapes both happen in one launch (the new token's row is read
- * from k_new / v_new by the workgroup that attends it and stored into the
- * cache in the same launch); other caches run the two launches.  The same
- * workspace as snap_decode_attn; k_new / v_new must not alias the cache. */
+ * contents as those two calls on the same stream.  For bf16 and fp8 caches of
+ * the GQA shapes (d_qk = d_v = 128) and bf16 latent caches both happen in one
+ * launch (the new token's row is read from k_new / v_new by the workgroup that
+ * attends it, quantised there for an fp8 cache, and stored into the cache in
+ * the same launch); other caches run the two launches.  The same workspace as
+ * snap_decode_attn; k_new / v_new must not alias the cache. */
 snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
                              const int32_t* n_topk, int32_t n, const int32_t* slot_ids,
                              const void* q, const void* k_new, const void* v_new, void* out,

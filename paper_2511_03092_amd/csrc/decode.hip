@@ -14,8 +14,8 @@
 //   decode_mla     fp8 latent rows, register-streamed
 //   decode_generic one wave per (chunk, sequence, query head); any dtype
 //   combine        log-sum-exp merge of the chunk partials -> out
-// For bf16 caches decode_mfma and decode_mla_lds also take the new token
-// (snap_decode_step): the append happens in the same launch.
+// decode_mfma (bf16 and fp8 caches) and decode_mla_lds (bf16) also take the
+// new token (snap_decode_step): the append happens in the same launch.
 #include <math.h>
 
 #include "snap_internal.h"
@@ -79,42 +79,6 @@ __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, i
   return true;
 }
 
-// Fused append: the cache row of the token at pos[slot] (the ring update of
-// Sec. III-C; sinks are filled in place while pos < sink), or -1 when the
-// launch carries no new token.  The row lies in the first run of valid rows,
-// so its virtual index equals its cache row.  The workgroup that owns it reads
-// it from k_new/v_new, chunk 0 stores it into the cache, and nothing else in
-// the launch touches that row: no ordering between workgroups is needed.
-__device__ __forceinline__ int new_row(const DecodeArgs& a, int slot) {
-  if (!a.k_new) return -1;
-  const int p = __builtin_amdgcn_readfirstlane(a.pos[slot]);
-  if (p < 0) return -1;
-  return p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
-}
-
-// Chunk 0 of (slot, KV head g) stores the new k (and v) row, one 16-byte
-// piece per thread (dk/8 + dv/8 pieces, at most the workgroup size).  The
-// piece is fetched with the query and stored once that load has landed, so
-// the store adds no memory round trip of its own.
-__device__ __forceinline__ bool new_piece_load(const DecodeArgs& a, int b, int g, int i, u32x4& x) {
-  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
-  if (i >= kc + vc) return false;
-  if (i < kc)
-    x = *((const u32x4*)a.k_new + ((size_t)b * a.Hkv + g) * kc + i);
-  else
-    x = *((const u32x4*)a.v_new + ((size_t)b * a.Hkv + g) * vc + (i - kc));
-  return true;
-}
-__device__ __forceinline__ void new_piece_store(const DecodeArgs& a, int g, int slot, int row, int i, u32x4 x) {
-  const int B = a.sink + a.recent + a.topk;
-  const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + row;
-  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
-  if (i < kc)
-    *((u32x4*)const_cast<void*>(a.ck) + crow * kc + i) = x;
-  else
-    *((u32x4*)const_cast<void*>(a.cv) + crow * vc + (i - kc)) = x;
-}
-
 // ---------------------------------------------------------------- fp8 -> bf16
 // 8 E4M3 codes -> 8 bf16 (exact: every E4M3 value is a bf16 value).  The
 // hardware conversion gives fp32; the bf16 is its upper half.
@@ -160,6 +124,73 @@ __device__ __forceinline__ u32x4 bf16x8_of(typename Raw8<FP8>::T r) {
     return r;
 }
 
+// 8 bf16 values (low half of each word first) -> the 8 E4M3 codes of
+// value / scale: the quantisation snap_cache_append stores.
+__device__ __forceinline__ u32x2 bf16x8_to_e4m3x8(u32x4 raw, float scale) {
+  u32x2 o;
+#pragma unroll
+  for (int h2 = 0; h2 < 2; ++h2) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = h2 * 4 + i;
+      const uint32_t bits = (j & 1) ? raw[j >> 1] >> 16 : raw[j >> 1] & 0xffffu;
+      w |= f32_to_e4m3(bf16_bits_to_f32(bits) / scale) << (8 * i);
+    }
+    o[h2] = w;
+  }
+  return o;
+}
+
+// The new token's 8 elements at `elem` of its bf16 input row, in the cache's
+// raw form: bf16 as is, fp8 quantised with the slot's scale (the bytes the
+// append writes, so attending them equals attending the appended row).
+template <bool FP8>
+__device__ __forceinline__ typename Raw8<FP8>::T new_raw8(const void* src, size_t elem, float scale) {
+  const u32x4 raw = *(const u32x4*)((const uint16_t*)src + elem);
+  if constexpr (FP8)
+    return bf16x8_to_e4m3x8(raw, scale);
+  else
+    return raw;
+}
+
+// Fused append: the cache row of the token at pos[slot] (the ring update of
+// Sec. III-C; sinks are filled in place while pos < sink), or -1 when the
+// launch carries no new token.  The row lies in the first run of valid rows,
+// so its virtual index equals its cache row.  The workgroup that owns it reads
+// it from k_new/v_new, chunk 0 stores it into the cache (fp8 caches: the
+// owning workgroup quantises it and stores the codes), and nothing else in the
+// launch touches that row: no ordering between workgroups is needed.
+__device__ __forceinline__ int new_row(const DecodeArgs& a, int slot) {
+  if (!a.k_new) return -1;
+  const int p = __builtin_amdgcn_readfirstlane(a.pos[slot]);
+  if (p < 0) return -1;
+  return p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
+}
+
+// Chunk 0 of (slot, KV head g) stores the new k (and v) row, one 16-byte
+// piece per thread (dk/8 + dv/8 pieces, at most the workgroup size).  The
+// piece is fetched with the query and stored once that load has landed, so
+// the store adds no memory round trip of its own.
+__device__ __forceinline__ bool new_piece_load(const DecodeArgs& a, int b, int g, int i, u32x4& x) {
+  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
+  if (i >= kc + vc) return false;
+  if (i < kc)
+    x = *((const u32x4*)a.k_new + ((size_t)b * a.Hkv + g) * kc + i);
+  else
+    x = *((const u32x4*)a.v_new + ((size_t)b * a.Hkv + g) * vc + (i - kc));
+  return true;
+}
+__device__ __forceinline__ void new_piece_store(const DecodeArgs& a, int g, int slot, int row, int i, u32x4 x) {
+  const int B = a.sink + a.recent + a.topk;
+  const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + row;
+  const int kc = a.dk / 8, vc = a.cv ? a.dv / 8 : 0;
+  if (i < kc)
+    *((u32x4*)const_cast<void*>(a.ck) + crow * kc + i) = x;
+  else
+    *((u32x4*)const_cast<void*>(a.cv) + crow * vc + (i - kc)) = x;
+}
+
 // ---------------------------------------------------------------- MFMA decode
 // KSTEPS = dk / 32, VPASS = dv / 128.  Lane l owns head l%16 of the group and,
 // per 16-row set, the output rows 4*(l/16)+e; P never leaves the lane between
@@ -195,11 +226,26 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   const float xs = a.scale * kLog2e * ksc;
   const void* vbase = a.cv ? a.cv : a.ck;
   const int vstride = a.cv ? a.dv : a.dk;
-  // fused append (bf16 only): row vnew comes from k_new / v_new
-  const int vnew = FP8 ? -1 : new_row(a, slot);
+  // fused append: row vnew comes from k_new / v_new (quantised for fp8 caches)
+  const int vnew = new_row(a, slot);
   const size_t knew_off = ((size_t)b * a.Hkv + g) * D, vnew_off = ((size_t)b * a.Hkv + g) * a.dv;
   u32x4 newp = {0u, 0u, 0u, 0u};
-  const bool has_newp = vnew >= 0 && chunk == 0 && new_piece_load(a, b, g, lane, newp);
+  const bool has_newp = !FP8 && vnew >= 0 && chunk == 0 && new_piece_load(a, b, g, lane, newp);
+  // fp8: the chunk that attends the new row quantises it once into LDS (K
+  // codes in pieces [0, D/8), V codes after them, 8 codes per piece) and
+  // stores those codes into the cache at its end
+  __shared__ u32x2 newq[FP8 ? (D + 128 * VPASS) / 8 : 1];
+  const bool owns_new = FP8 && vnew >= sp.v0 && vnew < sp.v1;
+  if constexpr (FP8) {
+    if (owns_new) {
+      constexpr int kc = D / 8;
+      if (lane < kc)
+        newq[lane] = new_raw8<true>(a.k_new, knew_off + 8 * lane, ksc);
+      else if (lane < kc + 16 * VPASS)
+        newq[lane] = new_raw8<true>(a.v_new, vnew_off + 8 * (lane - kc), vsc);
+      __syncthreads();
+    }
+  }
 
   float m = -INFINITY, mref = 0.f, lsum = 0.f;  // reference max (log2 units), its finite stand-in, sum
   f32x4 acc[VPASS][8];
@@ -226,15 +272,18 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
       return;
     }
     const int va = vb + l16, vb2 = vb + 16 + l16;
-    const void* pa = va == vnew ? a.k_new : a.ck;
-    const void* pb = vb2 == vnew ? a.k_new : a.ck;
-    const size_t ea = va == vnew ? knew_off : (row0 + virt_row(va, sp.n1, sr)) * D;
-    const size_t eb = vb2 == vnew ? knew_off : (row0 + virt_row(vb2, sp.n1, sr)) * D;
+    const size_t ea = (row0 + virt_row(va, sp.n1, sr)) * D;
+    const size_t eb = (row0 + virt_row(vb2, sp.n1, sr)) * D;
 #pragma unroll
     for (int t = 0; t < KSTEPS; ++t) {
       const int col = 8 * (KSTEPS * lg + t);
-      ka[t] = load_raw8<FP8>(pa, ea + col, va < sp.v1);
-      kb[t] = load_raw8<FP8>(pb, eb + col, vb2 < sp.v1);
+      if constexpr (FP8) {
+        ka[t] = va == vnew ? newq[col / 8] : load_raw8<FP8>(a.ck, ea + col, va < sp.v1);
+        kb[t] = vb2 == vnew ? newq[col / 8] : load_raw8<FP8>(a.ck, eb + col, vb2 < sp.v1);
+      } else {
+        ka[t] = load_raw8<FP8>(va == vnew ? a.k_new : a.ck, va == vnew ? knew_off + col : ea + col, va < sp.v1);
+        kb[t] = load_raw8<FP8>(vb2 == vnew ? a.k_new : a.ck, vb2 == vnew ? knew_off + col : eb + col, vb2 < sp.v1);
+      }
     }
   };
   RawT ka[KSTEPS], kb[KSTEPS];
@@ -256,10 +305,15 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
-        const void* pv = vi == vnew ? a.v_new : vbase;
-        const size_t ev = vi == vnew ? vnew_off : (row0 + virt_row(vi, sp.n1, sr)) * vstride;
+        const size_t ev = (row0 + virt_row(vi, sp.n1, sr)) * vstride;
 #pragma unroll
-        for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(pv, ev + 128 * pp + 8 * l16, vi < sp.v1);
+        for (int pp = 0; pp < VPASS; ++pp)
+          if constexpr (FP8)
+            vv[pp][i] = vi == vnew ? newq[D / 8 + 16 * pp + l16]
+                                   : load_raw8<FP8>(vbase, ev + 128 * pp + 8 * l16, vi < sp.v1);
+          else
+            vv[pp][i] = load_raw8<FP8>(vi == vnew ? a.v_new : vbase,
+                                       (vi == vnew ? vnew_off : ev) + 128 * pp + 8 * l16, vi < sp.v1);
       }
     }
     RawT kn[KSTEPS], kn2[KSTEPS];
@@ -335,6 +389,15 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
   if (has_newp) new_piece_store(a, g, slot, vnew, lane, newp);
+  if constexpr (FP8) {
+    if (owns_new && lane < D / 8 + 16 * VPASS) {
+      const size_t crow = ((size_t)slot * a.Hkv + g) * (size_t)B + vnew;
+      if (lane < D / 8)
+        *((u32x2*)const_cast<void*>(a.ck) + crow * (D / 8) + lane) = newq[lane];
+      else
+        *((u32x2*)const_cast<void*>(a.cv) + crow * (a.dv / 8) + (lane - D / 8)) = newq[lane];
+    }
+  }
   if (!hval) return;
   const size_t pi = ((size_t)b * a.Hq + qh) * a.n_chunks + chunk;
   if (lg == 0) a.ml[pi] = make_float2(m, lsum);
@@ -934,19 +997,12 @@ struct AppendArgs {
 
 template <typename In, typename Out>
 __device__ __forceinline__ void put8(const In* src, Out* dst, float scale) {
-  if constexpr (sizeof(Out) == 1) {
+  if constexpr (sizeof(Out) == 1 && sizeof(In) == 2) {
+    *(u32x2*)dst = bf16x8_to_e4m3x8(*(const u32x4*)src, scale);
+  } else if constexpr (sizeof(Out) == 1) {
     float f[8];
-    if constexpr (sizeof(In) == 2) {
-      u32x4 raw = *(const u32x4*)src;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f[2 * i] = bf16_bits_to_f32(raw[i] & 0xffffu);
-        f[2 * i + 1] = bf16_bits_to_f32(raw[i] >> 16);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) f[i] = ((const float*)src)[i];
-    }
+    for (int i = 0; i < 8; ++i) f[i] = ((const float*)src)[i];
     u32x2 o;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
@@ -1014,7 +1070,10 @@ Geometry decode_geometry(const snap_params& p, int n) {
   const bool latent_lds = latent && p.kv_dtype == SNAP_BF16;  // one 4-wave workgroup per CU (LDS-bound)
   const int target = latent_lds ? kLatentLdsWGs : (latent ? 512 : 2048);
   const int min_rows = latent ? 256 : 128;
-  int want = (target + units - 1) / units;
+  // rounded down: a grid just above the resident capacity would leave a
+  // partial second round of workgroups (measured 25% slower on the fp8 GQA
+  // kernel at 248 units: 9 chunks against 8)
+  int want = target / units;
   int maxc = (B + min_rows - 1) / min_rows;
   if (maxc < 1) maxc = 1;
   if (maxc > kMaxChunks) maxc = kMaxChunks;
@@ -1063,9 +1122,10 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
   const bool mla_ok = p.in_dtype == SNAP_BF16 && p.v_in_k && p.n_kv_heads == 1 && p.d_qk == 576 && p.d_v == 512 &&
                       (p.kv_dtype == SNAP_BF16 || p.kv_dtype == SNAP_FP8_E4M3);
   if (k_new) {
-    // the bf16 MFMA kernels take the new token in the same launch; the others
-    // run the append kernel first (same result)
-    if ((mla_ok || mfma_ok) && p.kv_dtype == SNAP_BF16) {
+    // the MFMA kernels (GQA: bf16 and fp8 caches; latent: bf16) take the new
+    // token in the same launch; the others run the append kernel first (same
+    // result)
+    if (mfma_ok || (mla_ok && p.kv_dtype == SNAP_BF16)) {
       a.k_new = k_new;
       a.v_new = p.v_in_k ? nullptr : v_new;
     } else {

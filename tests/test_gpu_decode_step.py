@@ -1,8 +1,8 @@
 """snap_decode_step (append + attend for one layer in one call) against the two
 calls it replaces, snap_cache_append then snap_decode_attn: outputs and cache
 bytes must be identical bit for bit at every step, and the fused outputs match
-the fp64 oracle.  Cases cover the fused kernels (bf16 GQA MFMA, bf16 latent)
-and the two-launch ones (fp8, fp32), a prompt shorter than the sinks (new
+the fp64 oracle.  Cases cover the fused kernels (bf16 and fp8 GQA MFMA, bf16
+latent) and the two-launch one (fp32), a prompt shorter than the sinks (new
 tokens land in sink rows), the ring wrapping, and an invalid slot id.
 
 Every case prints what names it before touching the GPU.
@@ -93,12 +93,12 @@ def test_step_latent_bf16_fused_kernel():
     print(f"  fused decode max abs err vs oracle: {err:.3e}", flush=True)
 
 
-def test_step_fp8_and_fp32_two_launch_paths():
+def test_step_fp8_fused_and_fp32_two_launch_paths():
     wl = synth.small(GQA, kv_dtype="fp8")
     p = params_of(wl)
-    lengths = [2000, 900]
-    _announce(f"decode_step fp8 GQA (append + attend launches): lengths {lengths}")
-    _fused_vs_two_calls(wl, p, lengths, [1, 0], 2, 24, torch.bfloat16)
+    lengths = [2000, 900, 3]
+    _announce(f"decode_step fp8 GQA (fused kernel, new row quantised in LDS): lengths {lengths}, one prompt < sinks")
+    _fused_vs_two_calls(wl, p, lengths, [1, 0, 2], 3, 24, torch.bfloat16, invalid_slot=True)
     wl = synth.WORKLOADS["tiny-fp32"]
     p = params_of(wl)
     _announce("decode_step fp32 tiny (generic kernel, two launches)")

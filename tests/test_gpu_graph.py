@@ -96,7 +96,13 @@ def test_graph_replay_latent_bf16():
     _graph_vs_eager(wl, params_of(wl), [3000, 1500], 6)
 
 
-def test_graph_replay_fp8_two_launch_path():
+def test_graph_replay_fp8_fused():
     wl = synth.small(GQA, kv_dtype="fp8")
-    print("\n[case] graph replay: fp8 GQA decode step (append + attend launches), 4 replays", flush=True)
+    print("\n[case] graph replay: fp8 GQA decode step (fused kernel + combine + advance), 4 replays", flush=True)
     _graph_vs_eager(wl, params_of(wl), [2000, 900], 4)
+
+
+def test_graph_replay_fp32_two_launch_path():
+    wl = synth.WORKLOADS["tiny-fp32"]
+    print("\n[case] graph replay: fp32 decode step (append + attend launches), 4 replays", flush=True)
+    _graph_vs_eager(wl, params_of(wl), [1024, 700], 4)
