@@ -619,14 +619,15 @@ struct ReduceArgs {
 // pass keeps m2 = max y and sum 2^(y - m2) with y = z*log2(e)).  The reference
 // c2 is 0 when the natural-log max lies in [-20, 64] (then 2^y is taken
 // directly, keeping the full fp32 accuracy of small logits), otherwise
-// c2 = m2; inv = 1 / sum_j 2^(y_j - c2), accumulated in fp64.  Eight lanes
-// share a row (chunks strided by 8) and combine with in-wave shuffles; block 0
-// of each group also resets the group's selection scratch.
-constexpr int kReduceLanes = 8;
+// c2 = m2; inv = 1 / sum_j 2^(y_j - c2), accumulated in fp64.  A wave owns a
+// row (chunks strided by 64, a few hundred at most) and combines with in-wave
+// shuffles; block 0 of each group also resets the group's selection scratch.
+constexpr int kReduceLanes = 64;
+constexpr int kReduceRows = 256 / kReduceLanes;  // rows per workgroup
 __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
   const int bg = bid_y(), b = bg / a.Hkv;
   const int sub = tid() % kReduceLanes;
-  const int rho = bid_x() * (256 / kReduceLanes) + tid() / kReduceLanes;
+  const int rho = bid_x() * kReduceRows + tid() / kReduceLanes;
   const float2* st = a.stats + (size_t)bg * a.n_kchunks * a.rows_pad;
   if (rho < a.rows_pad) {
     float m = -INFINITY;
@@ -1074,13 +1075,15 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   g.rows_pad = (g.rows + 31) / 32 * 32;
   int groups = n_seq * p.n_kv_heads;
   // Key chunks: enough workgroups to cover the 256 CUs several times (about
-  // 4096), but each chunk at least 16 * rows_pad keys, so that its keys
-  // outweigh the query fragments every workgroup loads first by 16x (the
-  // 256-row latent shape: 4096-key chunks; 128-row GQA: 2048).
+  // 4096), but each chunk at least 4 * rows_pad keys (16 * rows_pad for the
+  // wide latent groups, whose query block is 295 KB), so that its keys
+  // outweigh the query fragments every workgroup loads first (measured: the
+  // 256-row latent shape is fastest at 4096-key chunks; a single 128-row GQA
+  // prompt at 512-key chunks, 28% faster score passes than at 2048).
   long target = 4096;
   long per_group = (target + groups - 1) / (groups > 0 ? groups : 1);
   long kc = (max_len + per_group - 1) / (per_group > 0 ? per_group : 1);
-  const long kc_min = 16L * g.rows_pad;
+  const long kc_min = (g.rows_pad > 128 ? 16L : 4L) * g.rows_pad;
   if (kc < kc_min) kc = kc_min;
   kc = (kc + kKeyTile - 1) / kKeyTile * kKeyTile;
   if (kc > 16384) kc = 16384;
@@ -1206,7 +1209,8 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   ra.topk = p.topk;
   ra.rows_pad = geo.rows_pad;
   ra.n_kchunks = geo.n_kchunks;
-  hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + 31) / 32, groups), dim3(256), 0, stream, ra);
+  hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + kReduceRows - 1) / kReduceRows, groups), dim3(256), 0,
+                     stream, ra);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
 
   e = bf ? launch_score<uint16_t>(sa, p.d_qk, true, groups, geo.n_kchunks, stream)
