@@ -984,23 +984,35 @@ __device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff
   return m < keff ? sel[m] : -1;
 }
 
-// Copy 8 elements (16 bytes of bf16, 32 of fp32) of an input row into the
-// cache, quantising to E4M3 codes of x / scale when the cache is fp8; a NULL
-// source writes zeros.
+// 8 elements of an input row in raw form: 16 bytes of bf16 or 32 of fp32
+// (zeros for a NULL source, a padding row).
+template <typename In>
+struct Raw8In {
+  u32x4 w[sizeof(In) / 2];
+};
+template <typename In>
+__device__ __forceinline__ Raw8In<In> load8(const In* src) {
+  Raw8In<In> x;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(In) / 2); ++i)
+    x.w[i] = src ? *((const u32x4*)src + i) : u32x4{0u, 0u, 0u, 0u};
+  return x;
+}
+// ... stored into the cache, quantised to E4M3 codes of x / scale when the
+// cache is fp8.
 template <typename In, typename Out>
-__device__ __forceinline__ void copy8(const In* src, Out* dst, float scale) {
+__device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scale) {
   if constexpr (sizeof(Out) == 1) {
     float f[8];
     if constexpr (sizeof(In) == 2) {
-      u32x4 raw = src ? *(const u32x4*)src : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        f[2 * i] = bf16_bits_to_f32(raw[i] & 0xffffu);
-        f[2 * i + 1] = bf16_bits_to_f32(raw[i] >> 16);
+        f[2 * i] = bf16_bits_to_f32(x.w[0][i] & 0xffffu);
+        f[2 * i + 1] = bf16_bits_to_f32(x.w[0][i] >> 16);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) f[i] = src ? src[i] : 0.f;
+      for (int i = 0; i < 8; ++i) f[i] = __uint_as_float(x.w[i >> 2][i & 3]);
     }
     u32x2 o;
 #pragma unroll
@@ -1011,17 +1023,17 @@ __device__ __forceinline__ void copy8(const In* src, Out* dst, float scale) {
       o[h] = w;
     }
     *(u32x2*)dst = o;
-  } else if constexpr (sizeof(In) == 2) {
-    *(u32x4*)dst = src ? *(const u32x4*)src : u32x4{0u, 0u, 0u, 0u};
   } else {
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    *(u32x4*)dst = src ? *(const u32x4*)src : z;
-    *(u32x4*)((float*)dst + 4) = src ? *(const u32x4*)(src + 4) : z;
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(In) / 2); ++i) *((u32x4*)dst + i) = x.w[i];
   }
 }
 
 // Each workgroup rewrites rows_per_block cache rows of one (sequence, KV
-// head); threads walk (row, 8-element piece) pairs so every lane copies.
+// head); threads walk (row, 8-element piece) pairs so every lane copies, kAsmU
+// pairs at a time: their selected-index reads, then their row reads, are all
+// issued before the first store (two memory round trips per kAsmU pieces).
+constexpr int kAsmU = 8;
 template <typename In, typename Out>
 __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
@@ -1051,16 +1063,33 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const float vs = (sizeof(Out) == 1 && a.v) ? a.v_scale[(size_t)slot * a.Hkv + g] : 1.f;
   const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
   const int items = (row1 - row0) * per_row;
-  for (int it = tid(); it < items; it += nthreads()) {
-    const int row = row0 + it / per_row, piece = it % per_row;
-    const int t = row_source(row, L, s, r, keff, sg);
-    if (piece < kp) {
-      const In* src = t >= 0 ? (const In*)a.k + (in_row0 + t) * a.dk + 8 * piece : nullptr;
-      copy8<In, Out>(src, (Out*)a.ck + (out_row0 + row) * a.dk + 8 * piece, ks);
-    } else {
-      const int pv = piece - kp;
-      const In* src = t >= 0 ? (const In*)a.v + (in_row0 + t) * a.dv + 8 * pv : nullptr;
-      copy8<In, Out>(src, (Out*)a.cv + (out_row0 + row) * a.dv + 8 * pv, vs);
+  for (int it0 = tid(); it0 < items; it0 += kAsmU * nthreads()) {
+    int src_t[kAsmU];
+#pragma unroll
+    for (int u = 0; u < kAsmU; ++u) {
+      const int it = it0 + u * nthreads();
+      src_t[u] = it < items ? row_source(row0 + it / per_row, L, s, r, keff, sg) : -1;
+    }
+    Raw8In<In> x[kAsmU];
+#pragma unroll
+    for (int u = 0; u < kAsmU; ++u) {
+      const int it = it0 + u * nthreads();
+      const int piece = it % per_row, t = src_t[u];
+      const In* src = nullptr;
+      if (it < items && t >= 0)
+        src = piece < kp ? (const In*)a.k + (in_row0 + t) * a.dk + 8 * piece
+                         : (const In*)a.v + (in_row0 + t) * a.dv + 8 * (piece - kp);
+      x[u] = load8<In>(src);
+    }
+#pragma unroll
+    for (int u = 0; u < kAsmU; ++u) {
+      const int it = it0 + u * nthreads();
+      if (it >= items) break;
+      const int row = row0 + it / per_row, piece = it % per_row;
+      if (piece < kp)
+        store8<In, Out>(x[u], (Out*)a.ck + (out_row0 + row) * a.dk + 8 * piece, ks);
+      else
+        store8<In, Out>(x[u], (Out*)a.cv + (out_row0 + row) * a.dv + 8 * (piece - kp), vs);
     }
   }
 }
