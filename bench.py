@@ -475,56 +475,73 @@ def run_cb(args, wl):
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_value, comp_budget_s=10.0,
-                 dec_budget_s=2.0):
-    """The fp64 oracle, single-threaded on the host, on a bounded sample of the
-    same workload: compress units (one sequence x one KV head) at the longest
-    prompt, cycling over the KV heads, until about comp_budget_s of work, and
-    decode units (one sequence x one KV head x one step) over the cache that
-    built, until about dec_budget_s; extrapolated by unit counts to the timed
-    work: every prompt in comp_lengths compressed (scaled by its length) and
-    dsteps decode steps of dec_seqs sequences, every layer, for `tokens`
-    decoded tokens."""
+def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_value, dec_budget_s=1.0):
+    """The fp64 oracle on the host's cores, on a bounded sample of the same
+    workload: compress units (one sequence x one KV head) at the longest
+    prompt and decode units (one sequence x one KV head x one step) over the
+    cache one of them built, first on one thread, then on T threads at once
+    (T = the cores available, at most 16; independent units, the oracle's C
+    calls run in parallel).  Extrapolated by unit counts to the timed work:
+    every prompt in comp_lengths compressed (scaled by its length) and dsteps
+    decode steps of dec_seqs sequences, every layer, for `tokens` decoded
+    tokens.  `value` is the T-thread rate; the one-thread rate is beside it."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     import oracle
     import synth
 
+    T = max(1, min(os.cpu_count() or 1, 16))
     op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
                        p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
     L = max(comp_lengths)
     q, k, v = synth.prefill(wl, 0, 0, L, device="cpu")
     G = op.group
-    n_comp, t_all, res = 0, 0.0, None
-    while t_all < comp_budget_s and n_comp < 64:
-        g = n_comp % p.n_kv_heads
-        qg, kg = oracle.f64(q[g * G:(g + 1) * G]), oracle.f64(k[g])
-        vg = None if v is None else oracle.f64(v[g])
-        t = time.time()
-        r_ = oracle.compress_group(op, L, qg, kg, vg)
-        t_all += time.time() - t
-        res = res or r_
-        n_comp += 1
-    t_comp = t_all / n_comp
+    heads = [(oracle.f64(q[g * G:(g + 1) * G]), oracle.f64(k[g]), None if v is None else oracle.f64(v[g]))
+             for g in range(p.n_kv_heads)]
+
+    def comp_unit(i):
+        qg, kg, vg = heads[i % p.n_kv_heads]
+        return oracle.compress_group(op, L, qg, kg, vg)
+
+    t = time.time()
+    res = comp_unit(0)
+    t_comp1 = time.time() - t
     qd = np.random.default_rng(0).normal(size=(G, p.d_qk))
+
+    def dec_units(n):
+        for _ in range(n):
+            oracle.decode_attn_group(op, L, len(res.sel), qd, res.cache_k, res.cache_v)
+
     n_dec, t_all = 0, 0.0
     while t_all < dec_budget_s and n_dec < 4096:
         t = time.time()
-        oracle.decode_attn_group(op, L, len(res.sel), qd, res.cache_k, res.cache_v)
+        dec_units(1)
         t_all += time.time() - t
         n_dec += 1
-    t_dec = t_all / n_dec
+    t_dec1 = t_all / n_dec
+    with ThreadPoolExecutor(T) as ex:
+        t = time.time()
+        list(ex.map(comp_unit, range(T)))
+        t_compT = (time.time() - t) / T
+        per = max(1, n_dec // 2)
+        t = time.time()
+        list(ex.map(dec_units, [per] * T))
+        t_decT = (time.time() - t) / (T * per)
     units_comp = layers * len(comp_lengths) * p.n_kv_heads
     units_dec = layers * dec_seqs * p.n_kv_heads * dsteps
-    comp_s = sum(t_comp * (Lb / L) for Lb in comp_lengths) * layers * p.n_kv_heads
-    dec_s = t_dec * units_dec
-    val = tokens / (comp_s + dec_s)
-    return {"value": float(f"{val:.6g}"), "unit": "tok/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{n_comp} compress units (1 sequence x 1 KV head, L={L}) at {t_comp:.2f} s each and "
-                       f"{n_dec} decode units (1 sequence x 1 KV head x 1 step) at {t_dec * 1e3:.1f} ms each, "
-                       f"single thread; extrapolated to {units_comp} compress units (scaled by length) and "
-                       f"{units_dec} decode units for {tokens} tokens"),
-            "gpu_over_cpu": float(f"{gpu_value / val:.4g}")}
+    scale = sum(Lb / L for Lb in comp_lengths) * layers * p.n_kv_heads
+    val1 = tokens / (t_comp1 * scale + t_dec1 * units_dec)
+    valT = tokens / (t_compT * scale + t_decT * units_dec)
+    return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
+            "single_thread_value": float(f"{val1:.6g}"),
+            "sample": (f"compress units (1 sequence x 1 KV head, L={L}): 1 alone at {t_comp1:.2f} s, then {T} "
+                       f"on {T} threads at {t_compT:.2f} s each; decode units (1 sequence x 1 KV head x 1 "
+                       f"step): {n_dec} alone at {t_dec1 * 1e3:.1f} ms, then {T * per} on {T} threads at "
+                       f"{t_decT * 1e3:.2f} ms each; extrapolated to {units_comp} compress units (scaled by "
+                       f"length) and {units_dec} decode units for {tokens} tokens"),
+            "gpu_over_cpu": float(f"{gpu_value / valT:.4g}")}
 
 
 if __name__ == "__main__":
