@@ -112,6 +112,8 @@ def parse():
                     help="decode with snap_cache_append + snap_decode_attn instead of snap_decode_step")
     ap.add_argument("--graph", action="store_true",
                     help="run each step's decode phase as one captured HIP graph (replayed every step)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="continuous batching: run each step's compression and decode on two streams at once")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
     return ap.parse_args()
@@ -314,8 +316,10 @@ def run_cb(args, wl):
     """Continuous batching over wl.slots static cache slots (every layer has
     its own caches; slot metadata is shared).  All slots are filled first
     (untimed).  Step t then retires slot t mod slots: snap_compress of a new
-    prompt into it for every layer, then one decode step (snap_decode_step per
-    layer, snap_advance) over the other slots.  Prompts are prefixes, of a
+    prompt into it for every layer, and one decode step (snap_decode_step per
+    layer, snap_advance) over the other slots, one after the other (with
+    --overlap, on two streams at once: they touch disjoint slots).
+    Prompts are prefixes, of a
     seeded length in the workload's range, of one 128k-token K/V bank per
     layer resident in HBM, each with its own observation-window queries.  fp8
     cache scales are per (slot, KV head) amax / 448, set by this harness: the
@@ -371,52 +375,70 @@ def run_cb(args, wl):
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
 
-    def compress(i, slot):
+    def compress(i, slot, sp):
         for l in range(layers):
             kb, vb = banks[l]
             snap.snap_compress(p, caches[l][4], pos, ntop, slot_ids[slot:slot + 1], lens[i:i + 1],
-                               obsq[l][i:i + 1], kb, vb, wsc, stream=sptr)
+                               obsq[l][i:i + 1], kb, vb, wsc, stream=sp)
 
-    def decode(t, retired):
+    def decode(t, retired, sp):
         for l in range(layers):
             qd, kd, vd = dec[l]
             snap.snap_decode_step(p, caches[l][4], pos, ntop, live[retired], qd[t], kd[t], vd[t], out, wsd,
-                                  stream=sptr)
-        snap.snap_advance(pos, live[retired], stream=sptr)
+                                  stream=sp)
+        snap.snap_advance(pos, live[retired], stream=sp)
 
     for r in range(S):  # fill every slot
-        compress(r, r)
+        compress(r, r, sptr)
     torch.cuda.synchronize()
     t_setup = time.time() - t_setup
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration, dev)
 
-    def ev():
+    def ev(st):
         e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
+        e.record(st)
         return e
 
+    # The new prompt's compression and the other slots' decode step touch
+    # disjoint slots, so with --overlap they run on two streams at once.
+    # Across steps: the compression of step t rewrites a slot the decode of
+    # step t-1 used, and the decode of step t attends the slot compressed in
+    # step t-1.
+    overlap = args.overlap
+    s_c = torch.cuda.Stream() if overlap else stream
+    s_d = torch.cuda.Stream() if overlap else stream
     # host mirror of each slot's prompt length and position, for the bytes count
     slot_len = list(lengths[:S])
     slot_pos = list(lengths[:S])
     s_r, row_bytes = wl.sink + wl.recent, (wl.d_qk + wl.d_v) * (1 if wl.kv_dtype == "fp8" else 2)
     timing = {"compress": [], "decode": []}
     dec_bytes, timed_lengths = 0, []
-    t0 = t1 = None
+    t0 = t1 = prev_c = prev_d = None
     for t in range(n_steps):
         timed = t >= args.warmup
         if t == args.warmup:
             torch.cuda.synchronize()
-            t0 = ev()
+            t0 = ev(stream)
+            if overlap:
+                s_c.wait_event(t0)
+                s_d.wait_event(t0)
         r = t % S
         i = S + t
-        c0 = ev() if timed else None
-        compress(i, r)
-        c1 = ev() if timed else None
-        decode(t, r)
+        if overlap and prev_d is not None:
+            s_c.wait_event(prev_d)
+        c0 = ev(s_c)
+        compress(i, r, s_c.cuda_stream)
+        prev_c_next = ev(s_c)
+        if overlap and prev_c is not None:
+            s_d.wait_event(prev_c)
+        d0 = ev(s_d)
+        decode(t, r, s_d.cuda_stream)
+        prev_d = ev(s_d)
+        prev_c = prev_c_next
         if timed:
-            timing["compress"].append((c0, c1))
-            timing["decode"].append((c1, ev()))
+            timing["compress"].append((c0, prev_c))
+            timing["decode"].append((d0, prev_d))
             timed_lengths.append(lengths[i])
         slot_len[r] = slot_pos[r] = lengths[i]
         for x in range(S):
@@ -427,7 +449,10 @@ def run_cb(args, wl):
                 dec_bytes += layers * (wl.n_kv_heads * (min(slot_pos[x] + 1, s_r) + min(ncand, wl.topk)) * row_bytes
                                        + wl.n_kv_heads * 2 * 4)  # rows + the two scales
             slot_pos[x] += 1
-    t1 = ev()
+    if overlap:
+        stream.wait_event(prev_c)
+        stream.wait_event(prev_d)
+    t1 = ev(stream)
     torch.cuda.synchronize()
     K = args.steps
     ms_step = t0.elapsed_time(t1) / K
@@ -455,7 +480,7 @@ def run_cb(args, wl):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "launch": "eager",
+        "launch": "eager, compression and decode on two streams" if overlap else "eager, one stream",
         "config": {"workload": wl.name, "layers": layers, "slots": S, "decoded_per_step": nd,
                    "prompt_length_range": list(wl.length_range), "prompt_bank_tokens": Lmax,
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
