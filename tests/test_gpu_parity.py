@@ -28,7 +28,7 @@ def _announce(msg):
 
 
 def _run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
-              check_every=1, fp8_scales=False):
+              check_every=1, fp8_scales=False, band_rtol=BAND_RTOL):
     q, k, v = synth.prefill_batch(wl, layer, lengths, salt=salt, pad_value=pad_value)
     cache = GpuCache(p, n_slots)
     if fp8_scales:
@@ -42,7 +42,7 @@ def _run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=f
     stats = check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
     print(f"  swaps within tolerance: {stats['swaps']}, pooled max rel err: {stats['pooled_rel_err']:.3e}, "
           f"decision band: {stats['band_rel_err']:.3e}", flush=True)
-    assert stats["band_rel_err"] <= BAND_RTOL and stats["pooled_rel_err"] <= ALL_RTOL
+    assert stats["band_rel_err"] <= band_rtol and stats["pooled_rel_err"] <= ALL_RTOL
     err = 0.0
     if steps:
         err = decode_steps(p, wl, cache, slots, steps, out_dtype, tol, check_every=check_every, layer=layer,
@@ -100,6 +100,38 @@ def test_edge_lengths(topk):
     lengths = [0, 1, 3, s + 5, s + r, s + r + 1, s + r + topk, s + r + topk + 1, 90]
     _announce(f"edge lengths {lengths} topk={topk}")
     _run_case(wl, p, lengths, list(range(len(lengths))), len(lengths), 20, torch.float32, TOL["f32"])
+
+
+# Selection policies beside the default: StreamingLLM alone (no selected
+# rows), a SAGE-KV-like choice (the last query only, no pooling), and the
+# paper's two hyper-parameter presets (Table 6: Llama 768 sinks / 6400 selected
+# / 1024 recent; DeepSeek 512 / 512 / 31744; window 32, pool kernel 13).
+# With a single window row the pooled score of a key sums only G = 4 weights,
+# so the rounding of one logit (fp32 accumulation of 128 bf16 products, up to
+# ~1e-6 relative in its weight at these logit sizes) is not averaged down over
+# G*w rows as with w = 32: the pooled-score bound near the threshold is 3e-6
+# there.  The selection rule itself (swaps only within 1e-6) is unchanged.
+BAND_RTOL_ONE_ROW = 3e-6
+POLICIES = {
+    "streamingllm": (lambda: synth.small(MED, topk=0), [5000, 777, 3001], 24, 1, BAND_RTOL),
+    "sagekv-like": (lambda: synth.small(MED, obs_window=1, pool_kernel=1), [5000, 777, 3001], 24, 1,
+                    BAND_RTOL_ONE_ROW),
+    "table6-llama": (lambda: synth.small(synth.WORKLOADS["llama8b-1layer-32k"], sink=768, recent=1024, topk=6400,
+                                         pool_kernel=13), [32768, 9000], 8, 4, BAND_RTOL),
+    "table6-deepseek": (lambda: synth.small(synth.WORKLOADS["mla-8head-61layer-b16-128k"], sink=512, recent=31744,
+                                            topk=512, pool_kernel=13), [40000], 4, 2, BAND_RTOL),
+}
+
+
+@pytest.mark.parametrize("name", list(POLICIES))
+def test_selection_policies(name):
+    make, lengths, steps, every, band = POLICIES[name]
+    wl = make()
+    p = params_of(wl)
+    _announce(f"policy {name}: sink {wl.sink}, recent {wl.recent}, topk {wl.topk}, window {wl.obs_window}, "
+              f"pool kernel {wl.pool_kernel}, lengths {lengths}")
+    _run_case(wl, p, lengths, list(range(len(lengths))), len(lengths), steps, torch.bfloat16, TOL["bf16"],
+              check_every=every, band_rtol=band)
 
 
 def test_invalid_slots_are_skipped():
