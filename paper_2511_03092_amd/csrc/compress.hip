@@ -1041,7 +1041,7 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   const int s = a.sink, r = a.recent, B = s + r + a.topk;
   int L = uniform(a.lengths[b]);
   L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
-  const int keff = uniform(a.state[bg].keff);
+  const int keff = a.topk == 0 ? 0 : uniform(a.state[bg].keff);  // no selection ran when topk = 0
   const int32_t* sg = a.sel + (size_t)bg * a.topk;
   const int row0 = bid_x() * a.rows_per_block;
   const int row1 = min(row0 + a.rows_per_block, B);
@@ -1219,61 +1219,67 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   sa.scale2_lo = (float)((double)scale * 1.4426950408889634074 - (double)sa.scale2);
   const bool bf = p.in_dtype == SNAP_BF16;
   hipError_t e;
+  // With no selected rows (StreamingLLM alone) the cache is sinks and ring
+  // only: nothing is scored or selected (unless the pooled scores are asked
+  // for), the assembly is the whole call.
+  const bool select = p.topk > 0 || pooled_out;
 
-  e = bf ? launch_score<uint16_t>(sa, p.d_qk, false, groups, geo.n_kchunks, stream)
-         : launch_score<float>(sa, p.d_qk, false, groups, geo.n_kchunks, stream);
-  if (e != hipSuccess) return SNAP_ERR_HIP;
+  if (select) {
+    e = bf ? launch_score<uint16_t>(sa, p.d_qk, false, groups, geo.n_kchunks, stream)
+           : launch_score<float>(sa, p.d_qk, false, groups, geo.n_kchunks, stream);
+    if (e != hipSuccess) return SNAP_ERR_HIP;
 
-  ReduceArgs ra;
-  ra.stats = stats;
-  ra.rowref = rowref;
-  ra.lengths = lengths;
-  ra.hist = hist;
-  ra.state = state;
-  ra.groups = groups;
-  ra.Hkv = p.n_kv_heads;
-  ra.max_len = max_len;
-  ra.sink = p.sink;
-  ra.recent = p.recent;
-  ra.topk = p.topk;
-  ra.rows_pad = geo.rows_pad;
-  ra.n_kchunks = geo.n_kchunks;
-  hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + kReduceRows - 1) / kReduceRows, groups), dim3(256), 0,
-                     stream, ra);
-  if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+    ReduceArgs ra;
+    ra.stats = stats;
+    ra.rowref = rowref;
+    ra.lengths = lengths;
+    ra.hist = hist;
+    ra.state = state;
+    ra.groups = groups;
+    ra.Hkv = p.n_kv_heads;
+    ra.max_len = max_len;
+    ra.sink = p.sink;
+    ra.recent = p.recent;
+    ra.topk = p.topk;
+    ra.rows_pad = geo.rows_pad;
+    ra.n_kchunks = geo.n_kchunks;
+    hipLaunchKernelGGL(stats_reduce, dim3((geo.rows_pad + kReduceRows - 1) / kReduceRows, groups), dim3(256), 0,
+                       stream, ra);
+    if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
 
-  e = bf ? launch_score<uint16_t>(sa, p.d_qk, true, groups, geo.n_kchunks, stream)
-         : launch_score<float>(sa, p.d_qk, true, groups, geo.n_kchunks, stream);
-  if (e != hipSuccess) return SNAP_ERR_HIP;
+    e = bf ? launch_score<uint16_t>(sa, p.d_qk, true, groups, geo.n_kchunks, stream)
+           : launch_score<float>(sa, p.d_qk, true, groups, geo.n_kchunks, stream);
+    if (e != hipSuccess) return SNAP_ERR_HIP;
 
-  SelectArgs se;
-  se.A = A;
-  se.P = P;
-  se.pooled_out = pooled_out;
-  se.lengths = lengths;
-  se.hist = hist;
-  se.state = state;
-  se.counts = counts;
-  se.sel = sel;
-  se.groups = groups;
-  se.Hkv = p.n_kv_heads;
-  se.max_len = max_len;
-  se.sink = p.sink;
-  se.recent = p.recent;
-  se.topk = p.topk;
-  se.pool_kernel = p.pool_kernel;
-  se.pool = p.pool;
-  se.n_splits = geo.n_splits;
-  dim3 sgrid(geo.n_splits, groups);
-  hipLaunchKernelGGL(pool_hist0, sgrid, dim3(kSelThreads), 0, stream, se);
-  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 0);
-  hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 1);
-  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 1);
-  hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 2);
-  hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 2);
-  hipLaunchKernelGGL(select_count, sgrid, dim3(kSelThreads), 0, stream, se);
-  hipLaunchKernelGGL(select_write, sgrid, dim3(kSelThreads), 0, stream, se);
-  if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+    SelectArgs se;
+    se.A = A;
+    se.P = P;
+    se.pooled_out = pooled_out;
+    se.lengths = lengths;
+    se.hist = hist;
+    se.state = state;
+    se.counts = counts;
+    se.sel = sel;
+    se.groups = groups;
+    se.Hkv = p.n_kv_heads;
+    se.max_len = max_len;
+    se.sink = p.sink;
+    se.recent = p.recent;
+    se.topk = p.topk;
+    se.pool_kernel = p.pool_kernel;
+    se.pool = p.pool;
+    se.n_splits = geo.n_splits;
+    dim3 sgrid(geo.n_splits, groups);
+    hipLaunchKernelGGL(pool_hist0, sgrid, dim3(kSelThreads), 0, stream, se);
+    hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 0);
+    hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 1);
+    hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 1);
+    hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 2);
+    hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 2);
+    hipLaunchKernelGGL(select_count, sgrid, dim3(kSelThreads), 0, stream, se);
+    hipLaunchKernelGGL(select_write, sgrid, dim3(kSelThreads), 0, stream, se);
+    if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+  }
 
   AssembleArgs aa;
   aa.k = k;

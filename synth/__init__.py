@@ -102,6 +102,17 @@ WORKLOADS = {
         layers=32, batch=1, length=None, length_range=(4096, 131072), decode_steps=2000,
         rope=True, plant_frac=0.01, slots=32),
 }
+# Selection-policy variants of the 128k workloads: the paper's DeepSeek preset
+# (512 sinks, 512 selected, 31744 recent, pool kernel 13) on the latent shape;
+# a SAGE-KV-like choice (the last query only, no pooling) and StreamingLLM
+# alone (no selected rows) on the Llama batch.
+WORKLOADS["mla-deepseek-preset-61layer-b16-128k"] = replace(
+    WORKLOADS["mla-8head-61layer-b16-128k"], name="mla-deepseek-preset-61layer-b16-128k", sink=512, recent=31744,
+    topk=512, pool_kernel=13)
+WORKLOADS["llama8b-sagekv-32layer-b8-128k"] = replace(
+    WORKLOADS["llama8b-32layer-b8-128k"], name="llama8b-sagekv-32layer-b8-128k", obs_window=1, pool_kernel=1)
+WORKLOADS["llama8b-streamingllm-32layer-b8-128k"] = replace(
+    WORKLOADS["llama8b-32layer-b8-128k"], name="llama8b-streamingllm-32layer-b8-128k", topk=0)
 
 
 def seed_of(cfg: int, layer: int, slot: int, purpose: int, step: int = 0) -> int:

@@ -134,6 +134,28 @@ def test_selection_policies(name):
               check_every=every, band_rtol=band)
 
 
+def test_streamingllm_assembly_only():
+    """topk = 0 without the debug outputs: the call only assembles sinks and
+    ring (nothing is scored); cache bytes and metadata against the oracle's
+    assembly, then decode steps against the oracle."""
+    wl = synth.small(MED, topk=0)
+    p = params_of(wl)
+    lengths = [5000, 12, 3001]
+    _announce(f"streamingllm, assembly only: lengths {lengths}")
+    q, k, v = synth.prefill_batch(wl, 0, lengths, pad_value=float("nan"))
+    cache = GpuCache(p, 3)
+    gpu_compress(p, cache, q, k, v, lengths, [2, 0, 1], debug=False)
+    ck, cv = cache.host_values()
+    for b, (L, sl) in enumerate(zip(lengths, [2, 0, 1])):
+        assert int(cache.pos[sl]) == L and int(cache.n_topk[sl]) == 0
+        for g in range(p.n_kv_heads):
+            ek = oracle.assemble(L, p.sink, p.recent, 0, oracle.f64(k[b, g, :L]), np.zeros(0, np.int32))
+            ev = oracle.assemble(L, p.sink, p.recent, 0, oracle.f64(v[b, g, :L]), np.zeros(0, np.int32))
+            assert np.array_equal(ck[sl, g], ek) and np.array_equal(cv[sl, g], ev), (b, g)
+    err = decode_steps(p, wl, cache, [2, 0, 1], 24, torch.bfloat16, TOL["bf16"])
+    print(f"  decode max abs err over 24 steps: {err:.3e}", flush=True)
+
+
 def test_invalid_slots_are_skipped():
     wl = synth.small(EDGE, topk=16)
     p = params_of(wl)
