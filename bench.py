@@ -265,7 +265,7 @@ def main():
     G = wl.n_q_heads // wl.n_kv_heads
     score_flop = 0
     for L in lengths:
-        keys = max(L - s_r, 0)  # candidates: the normaliser domain of both passes
+        keys = max(L - s_r, 0) if wl.topk > 0 else 0  # candidates: the normaliser domain of both passes
         score_flop += wl.n_kv_heads * 2 * G * min(wl.obs_window, L) * wl.d_qk * keys
     score_tflops = 2 * score_flop / (comp_ms * 1e-3) / 1e12 if comp_ms > 0 else 0.0
     tokens = n * dsteps
