@@ -80,16 +80,15 @@ __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, i
 }
 
 // ---------------------------------------------------------------- fp8 -> bf16
-// 8 E4M3 codes -> 8 bf16 (exact: every E4M3 value is a bf16 value).  The
-// hardware conversion gives fp32; the bf16 is its upper half.
+// 8 E4M3 codes -> 8 bf16 (exact: every E4M3 value is a bf16 value), two codes
+// per conversion instruction (scale 1; the cache scale is applied after the
+// products).
 __device__ __forceinline__ u32x4 e4m3x8_to_bf16x8(u32x2 c) {
   u32x4 o;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(c[h], false);
-    auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(c[h], true);
-    o[2 * h] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
-    o[2 * h + 1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+    o[2 * h] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[h], 1.0f, false));
+    o[2 * h + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[h], 1.0f, true));
   }
   return o;
 }
