@@ -65,6 +65,15 @@ typedef enum {
   SNAP_NORM_ROW = 1   /* softmax over the whole causal row [0, i]          */
 } snap_norm;
 
+/* Who sets an fp8 cache's per-(slot, KV head) scales. */
+typedef enum {
+  SNAP_FP8_SCALES_GIVEN = 0, /* the caller, before compress / append           */
+  SNAP_FP8_SCALES_AMAX = 1   /* snap_compress: amax / 448 over the rows the
+                                compressed cache keeps (sinks, ring, selected;
+                                1 when they are all zero), for K and V apart;
+                                tokens appended later saturate at +-448 codes */
+} snap_fp8_scales;
+
 /* The method's hyper-parameters (Sec. III, Table 6's names). */
 typedef struct {
   int32_t n_q_heads;   /* query heads; a multiple of n_kv_heads                 */
@@ -85,6 +94,7 @@ typedef struct {
   int32_t kv_dtype;    /* cache storage: SNAP_F32, SNAP_BF16 (in_dtype == the
                           same) or SNAP_FP8_E4M3 (with SNAP_BF16 inputs)          */
   float sm_scale;      /* softmax scale; <= 0 means 1/sqrt(d_qk)                 */
+  int32_t fp8_scales;  /* snap_fp8_scales (fp8 caches; ignored otherwise)        */
 } snap_params;
 
 /* One layer's compressed cache (device memory, caller-owned, row-major):
@@ -92,7 +102,8 @@ typedef struct {
  *   v       [n_slots][n_kv_heads][B][d_v]   kv_dtype; NULL when v_in_k
  *   k_scale [n_slots][n_kv_heads] fp32      FP8 only: stored code * scale is
  *   v_scale [n_slots][n_kv_heads] fp32      the value; set by the caller before
- *                                           compress/append; NULL otherwise. */
+ *                                           compress/append, or by compress
+ *                                           (fp8_scales); NULL otherwise. */
 typedef struct {
   void* k;
   void* v;

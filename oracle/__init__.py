@@ -66,6 +66,8 @@ def _load():
     lib.oracle_e4m3_encode.restype = ctypes.c_uint8
     lib.oracle_quantize.argtypes = [_dp, i64, ctypes.c_float, _u8p]
     lib.oracle_quantize.restype = None
+    lib.oracle_fp8_scale.argtypes = [_dp, i64]
+    lib.oracle_fp8_scale.restype = ctypes.c_float
     _lib = lib
     return lib
 
@@ -285,6 +287,12 @@ def quantize(x, scale: float) -> np.ndarray:
     out = np.zeros(x.size, np.uint8)
     _load().oracle_quantize(_d(x), x.size, float(scale), out.ctypes.data_as(_u8p))
     return out
+
+
+def fp8_scale(x) -> float:
+    """Scale from the data: max |x| / 448 in fp32 (1 when x is all zero)."""
+    x = np.ascontiguousarray(f64(x)).reshape(-1)
+    return float(_load().oracle_fp8_scale(_d(x), x.size))
 
 
 def dequantize(codes, scale: float) -> np.ndarray:

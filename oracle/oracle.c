@@ -272,6 +272,21 @@ uint8_t oracle_e4m3_encode(float v) {
   return sign | (uint8_t)best;
 }
 
+/* A scale chosen from the data (not from the paper, which keeps bf16 caches):
+ * the largest magnitude among n values divided by 448, the largest E4M3
+ * magnitude, so that value maps to the top code and nothing saturates; 1 when
+ * every value is zero.  The division is an fp32 one, as a device computes it. */
+float oracle_fp8_scale(const double* x, int64_t n) {
+  double amax = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    double a = fabs(x[i]);
+    if (a > amax) amax = a;
+  }
+  if (amax == 0.0) return 1.0f;
+  float af = (float)amax;
+  return af / 448.0f;
+}
+
 /* Quantise n values with one scale, deciding each code in fp32 the way a
  * device kernel does: the fp32 quotient x / scale, then the encode above. */
 void oracle_quantize(const double* x, int64_t n, float scale, uint8_t* codes) {

@@ -22,6 +22,7 @@ SNAP_OK, SNAP_ERR_INVALID_ARG, SNAP_ERR_UNSUPPORTED, SNAP_ERR_WORKSPACE, SNAP_ER
 SNAP_F32, SNAP_BF16, SNAP_FP8_E4M3 = 0, 1, 2
 SNAP_POOL_MAX, SNAP_POOL_AVG = 0, 1
 SNAP_NORM_CAND, SNAP_NORM_ROW = 0, 1
+SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
 
 EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_compress", "snap_cache_append",
             "snap_decode_attn", "snap_decode_step", "snap_advance", "snap_status_str", "snap_last_error"]
@@ -30,7 +31,8 @@ EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_compress",
 class SnapParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_q_heads", "n_kv_heads", "d_qk", "d_v", "v_in_k", "sink", "recent", "topk",
-        "obs_window", "pool_kernel", "pool", "norm", "in_dtype", "kv_dtype")] + [("sm_scale", ctypes.c_float)]
+        "obs_window", "pool_kernel", "pool", "norm", "in_dtype", "kv_dtype")] + [("sm_scale", ctypes.c_float),
+                                                                                  ("fp8_scales", ctypes.c_int32)]
 
 
 class SnapCache(ctypes.Structure):
@@ -98,6 +100,7 @@ class Params:
     in_dtype: int = SNAP_BF16
     kv_dtype: int = SNAP_BF16
     sm_scale: float = 0.0
+    fp8_scales: int = SNAP_FP8_SCALES_GIVEN
 
     @property
     def budget(self) -> int:
@@ -106,7 +109,7 @@ class Params:
     def c(self) -> SnapParams:
         return SnapParams(self.n_q_heads, self.n_kv_heads, self.d_qk, self.d_v, int(self.v_in_k), self.sink,
                           self.recent, self.topk, self.obs_window, self.pool_kernel, self.pool, self.norm,
-                          self.in_dtype, self.kv_dtype, float(self.sm_scale))
+                          self.in_dtype, self.kv_dtype, float(self.sm_scale), int(self.fp8_scales))
 
 
 def _ptr(t) -> int | None:

@@ -48,6 +48,8 @@ static snap_status check_params(const snap_params* p) {
   if (p->pool != SNAP_POOL_MAX && p->pool != SNAP_POOL_AVG) return fail(SNAP_ERR_INVALID_ARG, "unknown pool type");
   if (p->norm != SNAP_NORM_CAND && p->norm != SNAP_NORM_ROW) return fail(SNAP_ERR_INVALID_ARG, "unknown norm");
   if (!isfinite(p->sm_scale)) return fail(SNAP_ERR_INVALID_ARG, "sm_scale must be finite");
+  if (p->fp8_scales != SNAP_FP8_SCALES_GIVEN && p->fp8_scales != SNAP_FP8_SCALES_AMAX)
+    return fail(SNAP_ERR_INVALID_ARG, "unknown fp8_scales mode");
   const bool dims_ok = (p->d_qk == 64 && p->d_v == 64) || (p->d_qk == 128 && p->d_v == 128) ||
                        (p->d_qk == 576 && p->d_v == 512);
   if (!dims_ok) return fail(SNAP_ERR_UNSUPPORTED, "(d_qk, d_v) must be (64,64), (128,128) or (576,512)");

@@ -958,8 +958,8 @@ struct AssembleArgs {
   const void* v;       // or NULL
   void* ck;            // [n_slots][Hkv][B][dk]
   void* cv;
-  const float* k_scale;
-  const float* v_scale;
+  float* k_scale;      // [n_slots][Hkv], fp8 only (written in SNAP_FP8_SCALES_AMAX mode)
+  float* v_scale;
   const int32_t* slot_ids;
   const int32_t* lengths;
   const int32_t* sel;  // [groups][topk]
@@ -967,8 +967,11 @@ struct AssembleArgs {
   int32_t* sel_out;    // optional [groups][topk]
   int32_t* pos;
   int32_t* n_topk;
-  int Hkv, max_len, sink, recent, topk, dk, dv, n_slots, rows_per_block;
+  float2* amax;        // [groups][n_rowblocks] (K, V) amax of the kept rows, or NULL
+  int Hkv, max_len, sink, recent, topk, dk, dv, n_slots, rows_per_block, n_rowblocks;
 };
+
+constexpr int kAsmRows = 64;  // cache rows per assemble workgroup
 
 // Source token of cache row `row` (or -1 for a zero padding row).
 __device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff, const int32_t* sel) {
@@ -1029,6 +1032,59 @@ __device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scal
   }
 }
 
+// Largest magnitude of one workgroup's values (LDS across the waves); every
+// thread gets it.
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* lds) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+  __syncthreads();
+  if ((tid() & 63) == 0) lds[tid() >> 6] = v;
+  __syncthreads();
+  v = 0;
+  for (int w = 0; w < (int)(nthreads() >> 6); ++w) v = max(v, lds[w]);
+  return v;
+}
+
+// fp8 scales from the data (SNAP_FP8_SCALES_AMAX): per (group, block of
+// rows_per_block cache rows) the largest |K| and |V| among the rows the block
+// keeps; padding rows add nothing.  bf16 magnitudes order like their bit
+// patterns, so the maxima are taken on the 15 low bits.
+__global__ __launch_bounds__(256) void fp8_amax(AssembleArgs a) {
+  __shared__ uint32_t lds[4];
+  const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
+  const int slot = uniform(a.slot_ids[b]);
+  if (slot < 0 || slot >= a.n_slots) return;
+  const int s = a.sink, r = a.recent, B = s + r + a.topk;
+  int L = uniform(a.lengths[b]);
+  L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
+  const int keff = a.topk == 0 ? 0 : uniform(a.state[bg].keff);
+  const int32_t* sg = a.sel + (size_t)bg * a.topk;
+  const int row0 = bid_x() * a.rows_per_block;
+  const int row1 = min(row0 + a.rows_per_block, B);
+  const size_t in_row0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
+  const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
+  const int items = (row1 - row0) * per_row;
+  uint32_t mk = 0, mv = 0;
+  for (int it = tid(); it < items; it += nthreads()) {
+    const int row = row0 + it / per_row, piece = it % per_row;
+    const int t = row_source(row, L, s, r, keff, sg);
+    if (t < 0) continue;
+    const u32x4 x = piece < kp ? *((const u32x4*)((const uint16_t*)a.k + (in_row0 + t) * a.dk) + piece)
+                               : *((const u32x4*)((const uint16_t*)a.v + (in_row0 + t) * a.dv) + (piece - kp));
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m = max(m, max(x[i] & 0x7fffu, (x[i] >> 16) & 0x7fffu));
+    if (piece < kp)
+      mk = max(mk, m);
+    else
+      mv = max(mv, m);
+  }
+  mk = block_max_u32(mk, lds);
+  mv = block_max_u32(mv, lds);
+  if (tid() == 0)
+    a.amax[(size_t)bg * a.n_rowblocks + bid_x()] = make_float2(bf16_bits_to_f32(mk), bf16_bits_to_f32(mv));
+}
+
 // Each workgroup rewrites rows_per_block cache rows of one (sequence, KV
 // head); threads walk (row, 8-element piece) pairs so every lane copies, kAsmU
 // pairs at a time: their selected-index reads, then their row reads, are all
@@ -1059,8 +1115,31 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
   }
   const size_t in_row0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
   const size_t out_row0 = ((size_t)slot * a.Hkv + g) * (size_t)B;
-  const float ks = (sizeof(Out) == 1) ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
-  const float vs = (sizeof(Out) == 1 && a.v) ? a.v_scale[(size_t)slot * a.Hkv + g] : 1.f;
+  float ks = 1.f, vs = 1.f;
+  if constexpr (sizeof(Out) == 1) {
+    if (a.amax) {
+      // scales from the group's amax over every row block: amax / 448, or 1
+      // when every kept value is zero; block 0 records them for decoding
+      __shared__ uint32_t lds[4];
+      uint32_t mk = 0, mv = 0;
+      for (int i = tid(); i < a.n_rowblocks; i += nthreads()) {
+        const float2 m = a.amax[(size_t)bg * a.n_rowblocks + i];
+        mk = max(mk, __float_as_uint(m.x));
+        mv = max(mv, __float_as_uint(m.y));
+      }
+      const float ak = __uint_as_float(block_max_u32(mk, lds));
+      const float av = __uint_as_float(block_max_u32(mv, lds));
+      ks = ak > 0.f ? ak / 448.f : 1.f;
+      vs = av > 0.f ? av / 448.f : 1.f;
+      if (bid_x() == 0 && tid() == 0) {
+        a.k_scale[(size_t)slot * a.Hkv + g] = ks;
+        if (a.v) a.v_scale[(size_t)slot * a.Hkv + g] = vs;
+      }
+    } else {
+      ks = a.k_scale[(size_t)slot * a.Hkv + g];
+      if (a.v) vs = a.v_scale[(size_t)slot * a.Hkv + g];
+    }
+  }
   const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
   const int items = (row1 - row0) * per_row;
   for (int it0 = tid(); it0 < items; it0 += kAsmU * nthreads()) {
@@ -1139,6 +1218,10 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   off = align256(off + (size_t)groups * g.n_splits * sizeof(uint2));
   g.off_sel = off;
   off = align256(off + (size_t)groups * (p.topk > 0 ? p.topk : 1) * sizeof(int32_t));
+  // per (group, assemble row block): amax of the kept K and V rows (fp8 scales)
+  g.n_rowblocks = (p.sink + p.recent + p.topk + kAsmRows - 1) / kAsmRows;
+  g.off_amax = off;
+  off = align256(off + (size_t)groups * g.n_rowblocks * sizeof(float2));
   g.compress_bytes = off;
   return g;
 }
@@ -1303,9 +1386,14 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   aa.dk = p.d_qk;
   aa.dv = p.d_v;
   aa.n_slots = c.n_slots;
-  aa.rows_per_block = 64;
-  const int B = p.sink + p.recent + p.topk;
-  dim3 agrid((B + aa.rows_per_block - 1) / aa.rows_per_block, groups);
+  aa.rows_per_block = kAsmRows;
+  aa.n_rowblocks = geo.n_rowblocks;
+  aa.amax = nullptr;
+  dim3 agrid(geo.n_rowblocks, groups);
+  if (p.kv_dtype == SNAP_FP8_E4M3 && p.fp8_scales == SNAP_FP8_SCALES_AMAX) {
+    aa.amax = (float2*)(w + geo.off_amax);
+    hipLaunchKernelGGL(fp8_amax, agrid, dim3(256), 0, stream, aa);
+  }
   if (p.kv_dtype == SNAP_FP8_E4M3) {
     if (bf)
       hipLaunchKernelGGL((assemble<uint16_t, uint8_t>), agrid, dim3(256), 0, stream, aa);

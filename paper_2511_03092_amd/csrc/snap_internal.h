@@ -104,7 +104,8 @@ struct Geometry {
   int key_chunk;    // keys per workgroup in the score passes
   int n_kchunks;    // score-pass chunks per (sequence, KV head)
   int n_splits;     // candidate splits per group in pool/select
-  size_t off_stats, off_rowref, off_A, off_P, off_hist, off_state, off_counts, off_sel;
+  int n_rowblocks;   // assemble row blocks per group
+  size_t off_stats, off_rowref, off_A, off_P, off_hist, off_state, off_counts, off_sel, off_amax;
   size_t compress_bytes;
   // decode
   int n_chunks;     // split-K chunks per (sequence, KV head)

@@ -198,6 +198,39 @@ def test_fp8_cache_continuous_batching_shape():
                          check_every=4)
 
 
+def test_fp8_scales_from_data():
+    """SNAP_FP8_SCALES_AMAX: compress sets each (slot, KV head) scale to the
+    oracle's data scale of the rows the cache keeps (K and V apart; the
+    scales the caller left are overwritten), the codes are the oracle's
+    quantisation with it (checked by check_compress), and decode steps that
+    append past the kept rows' range match the oracle.  One prompt is shorter
+    than sinks + ring (no candidates), one has every candidate kept."""
+    wl = synth.WORKLOADS["cb-fp8-llama8b-32slot"]
+    p = params_of(wl, fp8_scales=snap.SNAP_FP8_SCALES_AMAX)
+    s, r, K = p.sink, p.recent, p.topk
+    lengths = [9000, 20000, 1500, s + r + 100]
+    slots = [5, 2, 7, 0]
+    _announce(f"fp8 scales from the data: lengths {lengths} into slots {slots} of 8")
+    q, k, v = synth.prefill_batch(wl, 0, lengths, pad_value=float("nan"))
+    cache = GpuCache(p, 8)
+    cache.k_scale.fill_(3.0)
+    cache.v_scale.fill_(3.0)
+    sel, pooled = gpu_compress(p, cache, q, k, v, lengths, slots)
+    stats = check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
+    assert stats["band_rel_err"] <= BAND_RTOL
+    nt = cache.n_topk.cpu().numpy()
+    for b, (L, sl) in enumerate(zip(lengths, slots)):
+        for g in range(p.n_kv_heads):
+            used = sel[b, g, :nt[sl]]
+            for src, scales in ((k, cache.k_scale), (v, cache.v_scale)):
+                rows = oracle.assemble(L, s, r, K, oracle.f64(src[b, g, :L]), used)
+                assert float(scales[sl, g]) == oracle.fp8_scale(rows), (b, g)
+    untouched = [x for x in range(8) if x not in slots]
+    assert torch.all(cache.k_scale[untouched] == 3.0) and torch.all(cache.v_scale[untouched] == 3.0)
+    err = decode_steps(p, wl, cache, slots, 16, torch.bfloat16, TOL["fp8"], check_every=4)
+    print(f"  decode max abs err over 16 steps: {err:.3e}", flush=True)
+
+
 def test_mla_latent_cache_reduced_length():
     """Latent (MLA) cache: 8 heads share one 576-wide row, values are its first
     512 dims; the workload's split at a shorter prompt."""

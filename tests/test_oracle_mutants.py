@@ -58,6 +58,9 @@ MUTANTS = [
      "      z[j] = acc;\n      if (z[j] > m) m = z[j];\n    }\n    double Z = 0.0;\n    double* oh"),
     ("decode value dims transposed in pairs", "oh[d] += e * cv[(size_t)j * cv_width + d];",
      "oh[d] += e * cv[(size_t)j * cv_width + (d ^ 1)];"),
+    ("fp8 data scale from the largest positive value, not magnitude", "double a = fabs(x[i]);\n    if (a > amax)",
+     "double a = x[i];\n    if (a > amax)"),
+    ("fp8 data scale for the wrong top code", "return af / 448.0f;", "return af / 240.0f;"),
     ("e4m3 ties to odd", "(d == bestd && (c & 1) == 0)", "(d == bestd && (c & 1) == 1)"),
     ("e4m3 overflow to NaN instead of saturating", "if (a >= 448.0) return sign | 0x7E;",
      "if (a >= 464.0) return sign | 0x7F;"),

@@ -481,3 +481,28 @@ def test_quantize_uses_fp32_quotient():
     q32 = (x.astype(np.float32) / scale).astype(np.float32)
     lib = torch.tensor(np.clip(q32, -448, 448)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     np.testing.assert_array_equal(codes, lib)
+
+
+def test_fp8_scale_from_data():
+    """The data-chosen scale puts the largest magnitude on the top E4M3 code
+    (448) and nothing beyond it; with a largest magnitude of exactly 448 it is
+    1 and the codes are torch's plain cast; all-zero data gets scale 1."""
+    assert oracle.fp8_scale(np.zeros(7)) == 1.0
+    for trial in range(20):
+        x = rng.normal(size=500) * 10 ** rng.uniform(-3, 3)
+        x = x.astype(np.float32).astype(np.float64)
+        sc = oracle.fp8_scale(x)
+        codes = oracle.quantize(x, sc)
+        i = int(np.argmax(np.abs(x)))
+        assert codes[i] == (0xFE if x[i] < 0 else 0x7E), trial
+        # nothing saturates: every quotient is within 448, the largest on it
+        quo = np.abs(x.astype(np.float32) / np.float32(sc))
+        assert np.all(quo <= 448.0 * (1 + 2.0 ** -22)), trial
+        assert abs(quo[i] - 448.0) <= 448.0 * 2.0 ** -22, trial
+    x = rng.normal(size=400).astype(np.float32).astype(np.float64)
+    x = x / np.max(np.abs(x)) * 448.0
+    x[3] = -448.0
+    x = x.astype(np.float32).astype(np.float64)
+    assert oracle.fp8_scale(x) == 1.0
+    lib = torch.tensor(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(oracle.quantize(x, 1.0), lib)
