@@ -112,6 +112,8 @@ def parse():
                     help="decode with snap_cache_append + snap_decode_attn instead of snap_decode_step")
     ap.add_argument("--graph", action="store_true",
                     help="run each step's decode phase as one captured HIP graph (replayed every step)")
+    ap.add_argument("--fp8-scales-from-data", action="store_true",
+                    help="continuous batching: snap_compress sets the fp8 scales (amax / 448 of the kept rows)")
     ap.add_argument("--overlap", action="store_true",
                     help="continuous batching: run each step's compression and decode on two streams at once")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -340,7 +342,8 @@ def run_cb(args, wl):
     torch.cuda.set_device(dev)
     DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
     p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
-                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype])
+                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype],
+                    fp8_scales=snap.SNAP_FP8_SCALES_AMAX if args.fp8_scales_from_data else snap.SNAP_FP8_SCALES_GIVEN)
     B = p.budget
     Lmax = wl.max_len
     n_steps = args.warmup + args.steps
@@ -487,7 +490,9 @@ def run_cb(args, wl):
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "q_heads": wl.n_q_heads,
                    "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v, "kv_dtype": wl.kv_dtype,
                    "step": "compress one new prompt into the retired slot (every layer), then one decode "
-                           "step of the other slots"},
+                           "step of the other slots",
+                   "fp8_scales": "amax/448 of the kept rows, set by snap_compress" if args.fp8_scales_from_data
+                   else "amax/448 of the layer's prompt bank, set by the harness"},
         "decode_step_ms_per_call": round(dec_ms, 4),
         "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(nd / (dec_ms * layers * 1e-3), 1) if dec_ms > 0 else 0.0,
