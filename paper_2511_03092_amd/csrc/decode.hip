@@ -580,10 +580,11 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
 // bf16 latent caches (576-wide rows, values = first 512 dims).  One workgroup
 // of 4 waves per (chunk, sequence) streams blocks of 32 rows through a ring
 // of LDS stages with direct global->LDS loads, so three blocks (110 KB) are in
-// flight per CU while one is consumed.  Wave w computes partial logits over
-// its share of the 18 k-steps (5,5,4,4), the four partials are summed through
-// LDS in a fixed order, and wave w computes the value product for dims
-// [128w, 128w+128).
+// flight per CU while one is consumed.  Every wave forms the block's logits
+// over all 18 k-steps (the same sums in the same order in each wave: no
+// exchange or barrier between the two products; measured 2% faster than
+// splitting the k-steps over the waves and summing through LDS), and wave w
+// computes the value product for dims [128w, 128w+128).
 // LDS rows are 72 chunks of 16 bytes; chunk c of row r sits at slot
 // r*72 + (c ^ lat_swz(r)).  The row swizzle spreads the key-fragment reads
 // (one chunk of 16 consecutive rows) over the banks; the value reads
@@ -638,7 +639,6 @@ __device__ __forceinline__ void lat_barrier() {
 __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   constexpr int D = 576;
   __shared__ __align__(16) unsigned char stage[kLatStages][kLatBlockBytes];
-  __shared__ f32x4 sx[4][2][64];  // partial logits [wave][row set][lane]
   const int lane = tid() & 63, w = tid() >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
   const int chunk = bid_x(), b = bid_y();
@@ -651,10 +651,10 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   const bool hval = h < a.G;
   const int wu = __builtin_amdgcn_readfirstlane(w);
 
-  // wave w owns k-steps [kb, kb+kc) of the 18 (5,5,4,4); lane group lg holds
-  // dims 32*kb + 8*(kc*lg + t), t < kc
-  const int kb = mla_kbeg(wu), kc = mla_kcnt(wu);
-  bf16x8 qf[5];
+  // every wave forms the block's logits over all 18 k-steps itself (the same
+  // sums in the same order in each wave, so no exchange between waves);
+  // lane group lg holds dims 8*(18*lg + t) of k-step t
+  bf16x8 qf[kMlaKSteps];
   // this lane's share of every block load: (row, chunk) of its 9 slots
   int ld_r[kLatLoadsPerWave], ld_c[kLatLoadsPerWave], ld_off[kLatLoadsPerWave];
 #pragma unroll
@@ -732,9 +732,9 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
       lat_wait_vm<0>();
     lat_barrier();
 #pragma unroll
-    for (int t = 0; t < 5; ++t) {
+    for (int t = 0; t < kMlaKSteps; ++t) {
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (hval && t < kc) v = *(const u32x4*)(qdst + (size_t)h * kLatRowBytes + (32 * kb + 8 * (kc * lg + t)) * 2);
+      if (hval) v = *(const u32x4*)(qdst + (size_t)h * kLatRowBytes + 8 * (kMlaKSteps * lg + t) * 2);
       qf[t] = __builtin_bit_cast(bf16x8, v);
     }
     lat_barrier();  // every wave has its query fragments: the last stage is free
@@ -757,21 +757,13 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
 
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 5; ++t) {
-      if (t < kc) {
-        const int c = 4 * kb + kc * lg + t;
-        const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(l16, c) * 16));
-        const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(16 + l16, c) * 16));
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[t], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[t], s1, 0, 0, 0);
-      }
+    for (int t = 0; t < kMlaKSteps; ++t) {
+      const int c = kMlaKSteps * lg + t;
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(l16, c) * 16));
+      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const u32x4*)(st + (size_t)lat_slot(16 + l16, c) * 16));
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[t], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[t], s1, 0, 0, 0);
     }
-    // sum the four waves' partial logits in a fixed order (identical in every wave)
-    sx[w][0][lane] = s0;
-    sx[w][1][lane] = s1;
-    lat_barrier();
-    s0 = ((sx[0][0][lane] + sx[1][0][lane]) + sx[2][0][lane]) + sx[3][0][lane];
-    s1 = ((sx[0][1][lane] + sx[1][1][lane]) + sx[2][1][lane]) + sx[3][1][lane];
     // raw dot products; the scale (> 0) is applied to the block max and folded
     // into the exponent
     float x[8];
