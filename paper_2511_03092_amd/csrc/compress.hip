@@ -505,60 +505,6 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
         }
       }
     }
-  } else if constexpr (kBF16 && NW == 8) {
-    // Ring in ping-pong: waves 0-3 (group A) and 4-7 (group B; each SIMD
-    // holds one wave of each) run half a tile apart, two barriers per tile.
-    // In the first half of step i group A multiplies tile i while group B runs
-    // the softmax arithmetic of tile i-1; in the second half A runs tile i's
-    // arithmetic while B multiplies tile i.  So matrix and vector work of the
-    // two waves of a SIMD overlap instead of taking turns.  Past the first
-    // barrier of step i every wave is done reading tile i-1, so its stage
-    // takes tile i+STAGES-1; past the second, both groups' column partials of
-    // tile i-1 are in colbuf.
-    const bool grp_a = __builtin_amdgcn_readfirstlane(wave) < NW / 2;
-    f32x4 acc[TK / 16][2];
-    int tp = c0;  // first key of the tile this wave multiplied last
-    for (int i = 0; i <= nt; ++i) {
-      const int t = c0 + i * TK;
-      if (i < nt) wait_vm_dyn(min(nt - 1 - i, STAGES - 2) * nload);  // tile i has landed
-      lds_barrier();                                                 // ... for every wave
-      if (i + STAGES - 1 < nt)
-        issue_tile<CPR, NW, TK>(kbase, kRowBytes, t + (STAGES - 1) * TK, c1, &tiles[(i + STAGES - 1) % STAGES][0],
-                                wave, lane);
-      if (grp_a ? i < nt : i > 0) {
-        if (grp_a) {
-#pragma unroll
-          for (int sb = 0; sb < TK / 16; ++sb)
-            score_mma_sb<In, KSTEPS, TK>(&tiles[i % STAGES][0], qf, qlds, sb, wave, lane, wave_has_rows, acc[sb]);
-          tp = t;
-        } else {
-          float xv[2][4][TK / 16];
-#pragma unroll
-          for (int sb = 0; sb < TK / 16; ++sb)
-            score_epi_sb<NW, COLSUM, TK>(a, acc[sb], colbuf[(i - 1) & 1], sl, tp, c1, interior_of(tp), sb, wave,
-                                         lane, xv);
-          if (!COLSUM) score_stats_tile<TK>(sl, xv);
-        }
-      }
-      lds_barrier();
-      if constexpr (COLSUM) {
-        if (i > 0) colsum_finish<NW, TK>(a, colbuf[(i - 1) & 1], t - TK, c1, bg);
-      }
-      if (i < nt) {
-        if (grp_a) {
-          float xv[2][4][TK / 16];
-#pragma unroll
-          for (int sb = 0; sb < TK / 16; ++sb)
-            score_epi_sb<NW, COLSUM, TK>(a, acc[sb], colbuf[i & 1], sl, tp, c1, interior_of(tp), sb, wave, lane, xv);
-          if (!COLSUM) score_stats_tile<TK>(sl, xv);
-        } else {
-#pragma unroll
-          for (int sb = 0; sb < TK / 16; ++sb)
-            score_mma_sb<In, KSTEPS, TK>(&tiles[i % STAGES][0], qf, qlds, sb, wave, lane, wave_has_rows, acc[sb]);
-          tp = t;
-        }
-      }
-    }
   } else {
     // Ring, one barrier per tile: past the barrier of tile i every wave has
     // finished tile i-1, so its stage takes tile i+STAGES-1 right away and
