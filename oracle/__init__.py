@@ -60,6 +60,8 @@ def _load():
     lib.oracle_decode_attn.argtypes = [i32, i32, i32, i32, i32, i32, i32, i64, i32, dbl,
                                        _dp, _dp, _dp, _dp]
     lib.oracle_decode_attn.restype = None
+    lib.oracle_prefill_attn.argtypes = [i32, i32, i32, i64, dbl, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_prefill_attn.restype = None
     lib.oracle_e4m3_value.argtypes = [ctypes.c_uint8]
     lib.oracle_e4m3_value.restype = dbl
     lib.oracle_e4m3_encode.argtypes = [ctypes.c_float]
@@ -262,6 +264,61 @@ def decode_attn(p: Params, pos, ntopk, q, cache_k, cache_v=None) -> np.ndarray:
                 p, int(pos[b]), int(ntopk[b]), q[b, g * G:(g + 1) * G], cache_k[b, g],
                 None if cache_v is None else cache_v[b, g])
     return out
+
+
+def prefill_attn_group(p: Params, L: int, q, k, v, want_lse: bool = False):
+    """Causal attention of the G heads of one group over the first L positions:
+    q [G][>=L][dk], k [>=L][dk], v [>=L][dv] -> out [G][L][dv] (and the rows'
+    natural-log normalisers [G][L] when want_lse)."""
+    G = q.shape[0]
+    qq = np.ascontiguousarray(f64(q)[:, :L])
+    kk = np.ascontiguousarray(f64(k)[:L])
+    vv = np.ascontiguousarray(f64(v)[:L])
+    out = np.zeros((G, max(L, 1), p.d_v), np.float64)
+    lse = np.zeros((G, max(L, 1)), np.float64) if want_lse else None
+    if L > 0:
+        _load().oracle_prefill_attn(G, p.d_qk, p.d_v, L, float(p.scale), _d(qq), _d(kk), _d(vv), _d(out),
+                                    _d(lse) if want_lse else None)
+    out = out[:, :L]
+    return (out, lse[:, :L]) if want_lse else out
+
+
+def window_queries(p: Params, lengths, q) -> np.ndarray:
+    """The observation-window queries of a padded batch of prompt queries
+    q [n][Hq][max_len][dk]: row ii of sequence b is position L_b - w + ii
+    (zeros where that position is negative), shape [n][Hq][w][dk] (Sec. III-B.2)."""
+    q = f64(q)
+    n, Hq, _, dk = q.shape
+    w = p.obs_window
+    out = np.zeros((n, Hq, w, dk), np.float64)
+    for b in range(n):
+        L = int(lengths[b])
+        for ii in range(w):
+            i = L - w + ii
+            if i >= 0:
+                out[b, :, ii] = q[b, :, i]
+    return out
+
+
+def prefill_attn(p: Params, lengths, q, k, v, threads: int | None = None) -> list:
+    """Causal attention of a padded batch: q [n][Hq][max_len][dk], k/v [n][Hkv][max_len][d].
+    Returns, per sequence, out [Hq][L][dv] (fp64)."""
+    q, k, v = f64(q), f64(k), f64(v)
+    n, Hkv = k.shape[0], k.shape[1]
+    G = p.group
+    units = [(b, g) for b in range(n) for g in range(Hkv)]
+
+    def run(u):
+        b, g = u
+        return prefill_attn_group(p, int(lengths[b]), q[b, g * G:(g + 1) * G], k[b, g], v[b, g])
+
+    threads = threads or min(len(units), os.cpu_count() or 1)
+    if threads > 1 and len(units) > 1:
+        with ThreadPoolExecutor(threads) as ex:
+            res = list(ex.map(run, units))
+    else:
+        res = [run(u) for u in units]
+    return [np.concatenate([res[b * Hkv + g] for g in range(Hkv)], axis=0) for b in range(n)]
 
 
 def append(p: Params, pos, cache_k, cache_v, k_new, v_new=None):

@@ -58,6 +58,19 @@ MUTANTS = [
      "      z[j] = acc;\n      if (z[j] > m) m = z[j];\n    }\n    double Z = 0.0;\n    double* oh"),
     ("decode value dims transposed in pairs", "oh[d] += e * cv[(size_t)j * cv_width + d];",
      "oh[d] += e * cv[(size_t)j * cv_width + (d ^ 1)];"),
+    ("prefill row does not see its own key",
+     "for (int64_t j = 0; j <= i; ++j) {", "for (int64_t j = 0; j < i + (i == 0); ++j) {"),
+    ("prefill row sees the next key too",
+     "for (int64_t j = 0; j <= i; ++j) {", "for (int64_t j = 0; j <= i + (i + 1 < L); ++j) {"),
+    ("softmax scale dropped in prefill attention",
+     "        z[j] = sm_scale * acc;\n        if (z[j] > m) m = z[j];\n      }\n      double Z = 0.0;\n      double* oi",
+     "        z[j] = acc;\n        if (z[j] > m) m = z[j];\n      }\n      double Z = 0.0;\n      double* oi"),
+    ("prefill value dims transposed in pairs", "oi[d] += e * v[(size_t)j * dv + d];",
+     "oi[d] += e * v[(size_t)j * dv + (d ^ 1)];"),
+    ("prefill query rows read position-major", "const double* qi = q + ((size_t)h * L + i) * dk;",
+     "const double* qi = q + ((size_t)i * G + h) * dk;"),
+    ("prefill normaliser without the row max", "lse[(size_t)h * L + i] = m + log(Z);",
+     "lse[(size_t)h * L + i] = log(Z);"),
     ("fp8 data scale from the largest positive value, not magnitude", "double a = fabs(x[i]);\n    if (a > amax)",
      "double a = x[i];\n    if (a > amax)"),
     ("fp8 data scale for the wrong top code", "return af / 448.0f;", "return af / 240.0f;"),

@@ -506,3 +506,77 @@ def test_fp8_scale_from_data():
     assert oracle.fp8_scale(x) == 1.0
     lib = torch.tensor(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     np.testing.assert_array_equal(oracle.quantize(x, 1.0), lib)
+
+
+# ---------------------------------------------------------------- prefill attention
+def _prefill_case(G=3, L=37, dk=8, dv=6, scale=0.41, seed=7):
+    r = np.random.default_rng(seed)
+    p = Params(n_q_heads=G, n_kv_heads=1, d_qk=dk, d_v=dv, sink=2, recent=4, topk=5, obs_window=4,
+               pool_kernel=3, sm_scale=scale)
+    q = r.standard_normal((G, L, dk))
+    k = r.standard_normal((L, dk))
+    v = r.standard_normal((L, dv))
+    return p, q, k, v
+
+
+def test_prefill_attn_matches_library_sdpa():
+    """Causal attention of the prefill graph (Sec. IV-A, MHA kernel) against
+    torch's scaled_dot_product_attention in fp64 (the G heads share K and V),
+    and the rows' normalisers against torch.logsumexp of the masked logits."""
+    p, q, k, v = _prefill_case()
+    G, L = q.shape[0], q.shape[1]
+    out, lse = oracle.prefill_attn_group(p, L, q, k, v, want_lse=True)
+    qt, kt, vt = (torch.from_numpy(x) for x in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        qt[None], kt[None, None].expand(1, G, L, -1), vt[None, None].expand(1, G, L, -1), is_causal=True,
+        scale=p.sm_scale)[0]
+    np.testing.assert_allclose(out, ref.numpy(), rtol=1e-12, atol=1e-12)
+    z = p.sm_scale * torch.einsum("hid,jd->hij", qt, kt)
+    z = z.masked_fill(torch.ones(L, L, dtype=torch.bool).triu(1), float("-inf"))
+    np.testing.assert_allclose(lse, torch.logsumexp(z, dim=-1).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_prefill_first_row_and_equal_keys():
+    """Position 0 sees only itself: its output is v_0 exactly.  With every key
+    equal the softmax is uniform over the causal prefix: out_i is the mean of
+    v_0..v_i and the normaliser is z + log(i+1)."""
+    p, q, k, v = _prefill_case(L=23)
+    G, L = q.shape[0], q.shape[1]
+    out = oracle.prefill_attn_group(p, L, q, k, v)
+    for h in range(G):
+        assert np.array_equal(out[h, 0], v[0])
+    k_eq = np.repeat(k[:1], L, axis=0)
+    out, lse = oracle.prefill_attn_group(p, L, q, k_eq, v, want_lse=True)
+    means = np.cumsum(v, axis=0) / np.arange(1, L + 1)[:, None]
+    for h in range(G):
+        np.testing.assert_allclose(out[h], means, rtol=1e-12, atol=1e-12)
+        z = p.sm_scale * (q[h] @ k[0])
+        np.testing.assert_allclose(lse[h], z + np.log(np.arange(1, L + 1)), rtol=1e-12, atol=1e-12)
+
+
+def test_prefill_dominant_key_selects_its_value():
+    """A key far more aligned with every query than the rest (logit gap > 50)
+    takes all the weight of every row that can see it; rows before it average
+    only what precedes them."""
+    p, q, k, v = _prefill_case(L=30, scale=1.0)
+    G, L = q.shape[0], q.shape[1]
+    j0 = 11
+    k2 = k * 0.01
+    k2[j0] = 0.0
+    q2 = np.repeat(np.eye(p.d_qk)[:1][None], G, axis=0).repeat(L, axis=1) * 1.0
+    k2[j0, 0] = 60.0
+    out = oracle.prefill_attn_group(p, L, q2, k2, v)
+    for h in range(G):
+        np.testing.assert_allclose(out[h, j0:], np.repeat(v[j0:j0 + 1], L - j0, axis=0), atol=1e-20, rtol=1e-12)
+        assert not np.allclose(out[h, j0 - 1], v[j0])
+
+
+def test_window_queries_are_the_last_w_positions():
+    """Sec. III-B.2: Q_obs holds the queries of the last L_obs prompt tokens;
+    row w-1 is position L-1, and rows before position 0 are empty."""
+    p = Params(n_q_heads=2, n_kv_heads=1, d_qk=3, d_v=3, sink=1, recent=2, topk=1, obs_window=4, pool_kernel=1)
+    q = np.arange(2 * 9 * 3, dtype=np.float64).reshape(1, 2, 9, 3)
+    got = oracle.window_queries(p, [9], q)
+    assert np.array_equal(got[0], q[0, :, 5:9])
+    got = oracle.window_queries(p, [2], q)
+    assert np.array_equal(got[0, :, 2:], q[0, :, 0:2]) and not got[0, :, :2].any()
