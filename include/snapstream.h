@@ -159,6 +159,34 @@ snap_status snap_compress(const snap_params* p, const snap_cache* cache, int32_t
                           const void* k, const void* v, int32_t* sel_out, float* pooled_out,
                           void* workspace, size_t ws_bytes, void* stream);
 
+/* Bytes of workspace snap_prefill needs for n_seq sequences padded to
+ * max_len: the snap_compress workspace, the window queries and a transposed
+ * copy of V.  0 on invalid parameters. */
+size_t snap_prefill_workspace(const snap_params* p, int32_t n_seq, int32_t max_len);
+
+/* Prefill attention and compression in one call (Sec. IV-A's attention step
+ * followed by Sec. III-B, with the window scores' softmax statistics taken
+ * from the attention pass instead of a separate recompute, Sec. III-B.2).
+ *   1. out[b][h][i] = sum_{j <= i} softmax_j(sm_scale q[b][h][i].k[b][g][j])
+ *      v[b][g][j] for every position i < L (g = h / G), in bf16;
+ *   2. the compression of snap_compress with q_obs = the queries of the last
+ *      obs_window positions of q (same cache, pos, n_topk, sel_out and
+ *      pooled_out results).
+ * Arguments as snap_compress, except (device):
+ *   q   [n_seq][n_q_heads][max_len][d_qk] bf16 (rows >= L never read),
+ *   k   [n_seq][n_kv_heads][max_len][d_qk] bf16,
+ *   v   [n_seq][n_kv_heads][max_len][d_v]  bf16,
+ *   out [n_seq][n_q_heads][max_len][d_v]   bf16; rows >= L are not written,
+ *   workspace >= snap_prefill_workspace(p, n_seq, max_len) bytes, 256-byte
+ *             aligned; its contents on entry do not matter.
+ * Supported: in_dtype bf16, d_qk == d_v in {64, 128} (v_in_k = 0), and
+ * G = n_q_heads / n_kv_heads in {1, 2, 4, 8}; SNAP_ERR_UNSUPPORTED otherwise.
+ * out must not alias q, k or v.  n_seq == 0 is a no-op. */
+snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t* pos, int32_t* n_topk,
+                         int32_t n_seq, const int32_t* slot_ids, const int32_t* lengths, int32_t max_len,
+                         const void* q, const void* k, const void* v, void* out, int32_t* sel_out,
+                         float* pooled_out, void* workspace, size_t ws_bytes, void* stream);
+
 /* Decode KV update (Sec. III-C): for each of the n sequences, the new token's
  * keys/values k_new [n][n_kv_heads][d_qk] and v_new [n][n_kv_heads][d_v]
  * (in_dtype; v_new NULL when v_in_k) are written to row

@@ -60,7 +60,7 @@ def _load():
     lib.oracle_decode_attn.argtypes = [i32, i32, i32, i32, i32, i32, i32, i64, i32, dbl,
                                        _dp, _dp, _dp, _dp]
     lib.oracle_decode_attn.restype = None
-    lib.oracle_prefill_attn.argtypes = [i32, i32, i32, i64, dbl, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_prefill_attn.argtypes = [i32, i32, i32, i64, i64, i64, dbl, _dp, _dp, _dp, _dp, _dp]
     lib.oracle_prefill_attn.restype = None
     lib.oracle_e4m3_value.argtypes = [ctypes.c_uint8]
     lib.oracle_e4m3_value.restype = dbl
@@ -266,21 +266,26 @@ def decode_attn(p: Params, pos, ntopk, q, cache_k, cache_v=None) -> np.ndarray:
     return out
 
 
-def prefill_attn_group(p: Params, L: int, q, k, v, want_lse: bool = False):
+def prefill_attn_group(p: Params, L: int, q, k, v, want_lse: bool = False, rows=None):
     """Causal attention of the G heads of one group over the first L positions:
-    q [G][>=L][dk], k [>=L][dk], v [>=L][dv] -> out [G][L][dv] (and the rows'
-    natural-log normalisers [G][L] when want_lse)."""
+    q [G][>=L][dk], k [>=L][dk], v [>=L][dv] -> out [G][n][dv] for the query
+    positions rows = (i0, i1) (default every position, n = i1 - i0), and the
+    rows' natural-log normalisers [G][n] when want_lse."""
     G = q.shape[0]
+    i0, i1 = (0, L) if rows is None else rows
+    assert 0 <= i0 <= i1 <= L
     qq = np.ascontiguousarray(f64(q)[:, :L])
     kk = np.ascontiguousarray(f64(k)[:L])
     vv = np.ascontiguousarray(f64(v)[:L])
-    out = np.zeros((G, max(L, 1), p.d_v), np.float64)
-    lse = np.zeros((G, max(L, 1)), np.float64) if want_lse else None
-    if L > 0:
-        _load().oracle_prefill_attn(G, p.d_qk, p.d_v, L, float(p.scale), _d(qq), _d(kk), _d(vv), _d(out),
+    assert qq.shape[1] == L and kk.shape[0] == L and vv.shape[0] == L, "inputs shorter than L"
+    n = i1 - i0
+    out = np.zeros((G, max(n, 1), p.d_v), np.float64)
+    lse = np.zeros((G, max(n, 1)), np.float64) if want_lse else None
+    if n > 0:
+        _load().oracle_prefill_attn(G, p.d_qk, p.d_v, L, i0, i1, float(p.scale), _d(qq), _d(kk), _d(vv), _d(out),
                                     _d(lse) if want_lse else None)
-    out = out[:, :L]
-    return (out, lse[:, :L]) if want_lse else out
+    out = out[:, :n]
+    return (out, lse[:, :n]) if want_lse else out
 
 
 def window_queries(p: Params, lengths, q) -> np.ndarray:

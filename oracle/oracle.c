@@ -240,17 +240,20 @@ void oracle_decode_attn(int G, int dk, int dv, int ck_width, int cv_width, int s
 /* Causal self-attention over the whole prompt for one KV-head group: the
  * attention step of the prefill graph (Sec. IV-A, the MHA kernel that fuses
  * Q K^T, softmax and P V), whose last w query rows are the observation window
- * of Sec. III-B.2.  For each of the G query heads h and every position i < L:
- *   out[h][i] = sum_{j <= i} softmax_j(sm_scale q_{h,i}.k_j) v_j.
- * If lse is not NULL, lse[h][i] = log sum_{j <= i} exp(sm_scale q_{h,i}.k_j)
+ * of Sec. III-B.2.  For each of the G query heads h and every position i in
+ * [i0, i1) (0 <= i0 <= i1 <= L):
+ *   out[h][i - i0] = sum_{j <= i} softmax_j(sm_scale q_{h,i}.k_j) v_j.
+ * If lse is not NULL, lse[h][i - i0] = log sum_{j <= i} exp(sm_scale q_{h,i}.k_j)
  * (the row's natural-log normaliser).
- *   q : [G][L][dk], k : [L][dk], v : [L][dv], out : [G][L][dv], lse : [G][L]. */
-void oracle_prefill_attn(int G, int dk, int dv, int64_t L, double sm_scale,
-                         const double* q, const double* k, const double* v,
-                         double* out, double* lse) {
+ *   q : [G][L][dk], k : [L][dk], v : [L][dv], out : [G][i1-i0][dv],
+ *   lse : [G][i1-i0]. */
+void oracle_prefill_attn(int G, int dk, int dv, int64_t L, int64_t i0, int64_t i1,
+                         double sm_scale, const double* q, const double* k,
+                         const double* v, double* out, double* lse) {
+  int64_t n = i1 - i0;
   double* z = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
   for (int h = 0; h < G; ++h) {
-    for (int64_t i = 0; i < L; ++i) {
+    for (int64_t i = i0; i < i1; ++i) {
       const double* qi = q + ((size_t)h * L + i) * dk;
       double m = -INFINITY;
       for (int64_t j = 0; j <= i; ++j) {
@@ -260,7 +263,7 @@ void oracle_prefill_attn(int G, int dk, int dv, int64_t L, double sm_scale,
         if (z[j] > m) m = z[j];
       }
       double Z = 0.0;
-      double* oi = out + ((size_t)h * L + i) * dv;
+      double* oi = out + ((size_t)h * n + (i - i0)) * dv;
       for (int d = 0; d < dv; ++d) oi[d] = 0.0;
       for (int64_t j = 0; j <= i; ++j) {
         double e = exp(z[j] - m);
@@ -268,7 +271,7 @@ void oracle_prefill_attn(int G, int dk, int dv, int64_t L, double sm_scale,
         for (int d = 0; d < dv; ++d) oi[d] += e * v[(size_t)j * dv + d];
       }
       for (int d = 0; d < dv; ++d) oi[d] /= Z;
-      if (lse) lse[(size_t)h * L + i] = m + log(Z);
+      if (lse) lse[(size_t)h * n + (i - i0)] = m + log(Z);
     }
   }
   free(z);

@@ -6,8 +6,8 @@ used for device memory and the current stream.  If the library is missing the
 first call raises -- there is no other implementation behind these names.
 
 Functions keep the C names (include/snapstream.h):
-    snap_compress, snap_cache_append, snap_decode_attn, snap_decode_step, snap_advance,
-    snap_compress_workspace, snap_decode_workspace, snap_status_str
+    snap_compress, snap_prefill, snap_cache_append, snap_decode_attn, snap_decode_step, snap_advance,
+    snap_compress_workspace, snap_prefill_workspace, snap_decode_workspace, snap_status_str
 """
 from __future__ import annotations
 
@@ -24,7 +24,8 @@ SNAP_POOL_MAX, SNAP_POOL_AVG = 0, 1
 SNAP_NORM_CAND, SNAP_NORM_ROW = 0, 1
 SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
 
-EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_compress", "snap_cache_append",
+EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_prefill_workspace", "snap_compress",
+            "snap_prefill", "snap_cache_append",
             "snap_decode_attn", "snap_decode_step", "snap_advance", "snap_status_str", "snap_last_error"]
 
 
@@ -66,6 +67,10 @@ def lib() -> ctypes.CDLL:
     L.snap_decode_workspace.restype = sz
     L.snap_compress.argtypes = [P, C, vp, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     L.snap_compress.restype = ctypes.c_int
+    L.snap_prefill_workspace.argtypes = [P, i32, i32]
+    L.snap_prefill_workspace.restype = sz
+    L.snap_prefill.argtypes = [P, C, vp, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.snap_prefill.restype = ctypes.c_int
     L.snap_cache_append.argtypes = [P, C, vp, i32, vp, vp, vp, vp]
     L.snap_cache_append.restype = ctypes.c_int
     L.snap_decode_attn.argtypes = [P, C, vp, vp, i32, vp, vp, vp, i32, vp, sz, vp]
@@ -152,6 +157,19 @@ def snap_compress(p: Params, cache: SnapCache, pos, n_topk, slot_ids, lengths, q
                                _ptr(slot_ids), _ptr(lengths), max_len, _ptr(q_obs), _ptr(k), _ptr(v),
                                _ptr(sel_out), _ptr(pooled_out), _ptr(workspace),
                                workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def snap_prefill_workspace(p: Params, n_seq: int, max_len: int) -> int:
+    return int(lib().snap_prefill_workspace(ctypes.byref(p.c()), n_seq, max_len))
+
+
+def snap_prefill(p: Params, cache: SnapCache, pos, n_topk, slot_ids, lengths, q, k, v, out, workspace,
+                 sel_out=None, pooled_out=None, stream=None):
+    n_seq, max_len = int(k.shape[0]), int(k.shape[2])
+    _check(lib().snap_prefill(ctypes.byref(p.c()), ctypes.byref(cache), _ptr(pos), _ptr(n_topk), n_seq,
+                              _ptr(slot_ids), _ptr(lengths), max_len, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                              _ptr(sel_out), _ptr(pooled_out), _ptr(workspace),
+                              workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def snap_cache_append(p: Params, cache: SnapCache, pos, slot_ids, k_new, v_new=None, stream=None):

@@ -107,6 +107,10 @@ struct Geometry {
   int n_rowblocks;   // assemble row blocks per group
   size_t off_stats, off_rowref, off_A, off_P, off_hist, off_state, off_counts, off_sel, off_amax;
   size_t compress_bytes;
+  // prefill (compress workspace followed by the window queries and V^T)
+  int ld_vt;        // keys per V^T row (max_len rounded up to the key tile)
+  size_t off_qobs, off_vt;
+  size_t prefill_bytes;
   // decode
   int n_chunks;     // split-K chunks per (sequence, KV head)
   size_t off_part, off_ml;
@@ -129,12 +133,19 @@ struct RadixState {
 
 Geometry compress_geometry(const snap_params& p, int n_seq, int max_len);
 Geometry decode_geometry(const snap_params& p, int n);
+Geometry prefill_geometry(const snap_params& p, int n_seq, int max_len);
 
 snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* pos,
                             int32_t* n_topk, int n_seq, const int32_t* slot_ids,
                             const int32_t* lengths, int max_len, const void* q_obs, const void* k,
                             const void* v, int32_t* sel_out, float* pooled_out, void* ws,
-                            hipStream_t stream);
+                            hipStream_t stream, bool stats_given = false);
+// causal attention of the whole prompt into out, then the compression with
+// the window statistics taken from the attention pass
+snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* pos, int32_t* n_topk, int n_seq,
+                           const int32_t* slot_ids, const int32_t* lengths, int max_len, const void* q, const void* k,
+                           const void* v, void* out, int32_t* sel_out, float* pooled_out, void* ws,
+                           hipStream_t stream);
 snap_status launch_append(const snap_params& p, const snap_cache& c, const int32_t* pos, int n,
                           const int32_t* slot_ids, const void* k_new, const void* v_new,
                           hipStream_t stream);

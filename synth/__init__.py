@@ -22,7 +22,7 @@ POOL_MAX, POOL_AVG = 0, 1
 NORM_CAND, NORM_ROW = 0, 1
 
 # purposes mixed into every seed so each tensor has its own stream
-P_Q, P_K, P_V, P_PLANT_POS, P_PLANT_DIR, P_DEC_Q, P_DEC_K, P_DEC_V, P_LEN = range(9)
+P_Q, P_K, P_V, P_PLANT_POS, P_PLANT_DIR, P_DEC_Q, P_DEC_K, P_DEC_V, P_LEN, P_Q_ALL = range(10)
 
 
 @dataclass(frozen=True)
@@ -233,6 +233,37 @@ def prefill_batch(wl: Workload, layer: int, lengths, device="cpu", salt: int = 0
         k[b] = kb
         if v is not None:
             v[b] = vb
+    return q, k, v
+
+
+def prompt_queries(wl: Workload, layer: int, slot: int, L: int, device="cpu", salt: int = 0,
+                   max_len: int | None = None, pad_value: float = 0.0) -> torch.Tensor:
+    """The queries of every prompt position, q [Hq][Lpad][dqk] (the input of the
+    prefill attention; its last w rows are that prompt's observation window),
+    Gaussian with the rotary encoding of positions 0..L-1; rows >= L hold
+    pad_value."""
+    Lpad = max_len or L
+    q = _randn((wl.n_q_heads, L, wl.d_qk), seed_of(wl.cfg_id, layer, slot, P_Q_ALL, salt), device)
+    if wl.rope:
+        rope_(q, torch.arange(L, device=device), wl.rope_theta)
+    qq = torch.full((wl.n_q_heads, Lpad, wl.d_qk), pad_value, dtype=torch.float32, device=device)
+    qq[:, :L] = q
+    return cast(qq, wl.in_dtype)
+
+
+def prompt_batch(wl: Workload, layer: int, lengths, device="cpu", salt: int = 0,
+                 max_len: int | None = None, pad_value: float = 0.0, slots=None):
+    """Padded batch for the prefill attention: q [n][Hq][max_len][dqk] (every
+    position), k [n][Hkv][max_len][dqk], v [n][Hkv][max_len][dv]; k and v as
+    prefill_batch draws them."""
+    n = len(lengths)
+    Lmax = max_len or max(lengths)
+    slots = list(range(n)) if slots is None else list(slots)
+    _, k, v = prefill_batch(wl, layer, lengths, device, salt, Lmax, pad_value, slots)
+    dt = torch.float32 if wl.in_dtype == "f32" else torch.bfloat16
+    q = torch.empty((n, wl.n_q_heads, Lmax, wl.d_qk), dtype=dt, device=device)
+    for b, L in enumerate(lengths):
+        q[b] = prompt_queries(wl, layer, slots[b], int(L), device, salt, Lmax, pad_value)
     return q, k, v
 
 

@@ -160,3 +160,38 @@ def test_decode_step_validation():
     lcache = snap.SnapCache(FAKE, None, None, None, 4)
     assert step(params=lat, c=lcache, ws_bytes=16) == snap.SNAP_ERR_WORKSPACE   # v_new ignored, then ws
     assert b"workspace" in snap.lib().snap_last_error()
+
+
+def test_prefill_validation():
+    """snap_prefill: the shapes it supports, its workspace and pointer checks,
+    all before any launch."""
+    L = snap.lib()
+    p = _params()
+    cache = snap.SnapCache(FAKE, FAKE, None, None, 4)
+    need = snap.snap_prefill_workspace(p, 1, 4096)
+    # the compress workspace plus the window queries and the transposed V
+    assert need >= snap.snap_compress_workspace(p, 1, 4096) + 32 * 32 * 128 * 2 + 8 * 128 * 4096 * 2
+    assert snap.snap_prefill_workspace(_params(pool_kernel=4), 1, 100) == 0
+
+    def pre(params=p, q=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 34, n_seq=1, max_len=4096):
+        return L.snap_prefill(ctypes.byref(params.c()), ctypes.byref(cache), FAKE, FAKE, n_seq, FAKE, FAKE, max_len,
+                              q, k, v, out, None, None, ws, ws_bytes, None)
+
+    assert pre(out=None) == snap.SNAP_ERR_INVALID_ARG
+    assert pre(out=FAKE + 2) == snap.SNAP_ERR_INVALID_ARG
+    assert pre(v=None) == snap.SNAP_ERR_INVALID_ARG
+    assert pre(q=FAKE + 8) == snap.SNAP_ERR_INVALID_ARG
+    assert pre(ws_bytes=need - 1) == snap.SNAP_ERR_WORKSPACE
+    assert pre(ws=FAKE + 64) == snap.SNAP_ERR_WORKSPACE
+    assert pre(n_seq=0) == snap.SNAP_OK
+    assert pre(max_len=0) == snap.SNAP_ERR_INVALID_ARG
+    # unsupported shapes and dtypes
+    assert pre(params=_params(in_dtype=snap.SNAP_F32, kv_dtype=snap.SNAP_F32)) == snap.SNAP_ERR_UNSUPPORTED
+    assert pre(params=_params(n_q_heads=48, n_kv_heads=4)) == snap.SNAP_ERR_UNSUPPORTED  # G = 12
+    assert pre(params=_params(n_q_heads=16, n_kv_heads=1, obs_window=16)) == snap.SNAP_ERR_UNSUPPORTED  # G = 16
+    lat = _params(n_q_heads=8, n_kv_heads=1, d_qk=576, d_v=512, v_in_k=1, recent=4096, topk=28668)
+    lcache = snap.SnapCache(FAKE, None, None, None, 4)
+    assert L.snap_prefill(ctypes.byref(lat.c()), ctypes.byref(lcache), FAKE, FAKE, 1, FAKE, FAKE, 4096, FAKE, FAKE,
+                          None, FAKE, None, None, FAKE, 1 << 34, None) == snap.SNAP_ERR_UNSUPPORTED
+    # a supported fp8 cache still needs its scales
+    assert pre(params=_params(kv_dtype=snap.SNAP_FP8_E4M3)) == snap.SNAP_ERR_INVALID_ARG

@@ -1,0 +1,186 @@
+"""GPU parity of snap_prefill (causal prefill attention with the SnapKV window
+statistics taken from the attention pass, then the compression) against the
+fp64 oracle: the attention output of every position, and the compression
+result (selection, pooled scores, cache bytes, metadata) for the observation
+window formed by the last w prompt queries.
+
+Every case prints what names it before touching the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2511_03092_amd as snap
+import synth
+from snaphelp import TOL, GpuCache, check_compress, check_selection, oracle_params, params_of
+
+pytestmark = pytest.mark.gpu
+
+# the same derived pooled-score bounds as the snap_compress parity tests
+BAND_RTOL = 1e-6
+ALL_RTOL = 1e-5
+
+# 8 query heads over 2 KV heads (G = 4, the Llama grouping), D = 128
+GQA = synth.Workload("prefill-gqa", 14, 8, 2, 128, 128, False, 4, 32, 100, 32, 7, "bf16", "bf16", layers=1, batch=4,
+                     length=None, length_range=(64, 1000), decode_steps=0, rope=True, plant_frac=0.01)
+
+
+def _announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def _gpu_prefill(p, wl, lengths, slots, n_slots, max_len=None, salt=0):
+    q, k, v = synth.prompt_batch(wl, 0, lengths, salt=salt, max_len=max_len, pad_value=float("nan"), slots=slots)
+    dev = "cuda"
+    n, ml = k.shape[0], k.shape[2]
+    cache = GpuCache(p, n_slots)
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.tensor(slots, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    # canary: rows at or past each prompt's length must stay untouched
+    out = torch.full((n, p.n_q_heads, ml, p.d_v), float("nan"), dtype=torch.bfloat16, device=dev)
+    sel = torch.empty((n, p.n_kv_heads, max(p.topk, 1)), dtype=torch.int32, device=dev)
+    pooled = torch.empty((n, p.n_kv_heads, ml), dtype=torch.float32, device=dev)
+    snap.snap_prefill(p, cache.c(), cache.pos, cache.n_topk, sl, lens, qd, kd, vd, out, ws, sel, pooled)
+    torch.cuda.synchronize()
+    return q, k, v, cache, out, sel.cpu().numpy(), pooled.cpu().numpy()
+
+
+def _check_attention(p, lengths, q, k, v, out):
+    op = oracle_params(p)
+    exp = oracle.prefill_attn(op, lengths, q, k, v)
+    worst = 0.0
+    for b, L in enumerate(lengths):
+        got = out[b, :, :L].double().cpu().numpy()
+        err = float(np.max(np.abs(got - exp[b]))) if L else 0.0
+        worst = max(worst, err)
+        assert err <= TOL["bf16"], (b, L, err)
+        assert torch.all(torch.isnan(out[b, :, L:].float())), f"rows past L={L} written"
+    return worst
+
+
+def _run(wl, p, lengths, slots=None, n_slots=None, band_rtol=BAND_RTOL):
+    slots = list(range(len(lengths))) if slots is None else slots
+    n_slots = len(lengths) if n_slots is None else n_slots
+    q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, slots, n_slots)
+    err = _check_attention(p, lengths, q, k, v, out)
+    qobs = oracle.window_queries(oracle_params(p), lengths, q)
+    st = check_compress(p, cache, qobs, k, v, lengths, slots, sel, pooled)
+    print(f"  attention max abs err {err:.3e}; swaps {st['swaps']}, pooled max rel err "
+          f"{st['pooled_rel_err']:.3e}, decision band {st['band_rel_err']:.3e}", flush=True)
+    assert st["band_rel_err"] <= band_rtol and st["pooled_rel_err"] <= ALL_RTOL
+    return st
+
+
+@pytest.mark.parametrize("norm", [synth.NORM_CAND, synth.NORM_ROW])
+def test_prefill_gqa_ragged_batch(norm):
+    wl = synth.small(GQA, norm=norm)
+    p = params_of(wl)
+    lengths = [1000, 333, 97, 1]
+    _announce(f"snap_prefill G=4 D=128 norm={'cand' if norm == 0 else 'row'}: lengths {lengths} (ragged tiles, "
+              "one prompt of one token)")
+    _run(wl, p, lengths, slots=[2, 0, 3, 1], n_slots=5)
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 64), (8, 4, 64), (8, 1, 64), (16, 2, 128)])
+def test_prefill_group_sizes(hq, hkv, d):
+    wl = synth.small(GQA, n_q_heads=hq, n_kv_heads=hkv, d_qk=d, d_v=d, obs_window=16)
+    p = params_of(wl)
+    lengths = [777, 130]
+    _announce(f"snap_prefill Hq={hq} Hkv={hkv} (G={hq // hkv}) D={d}: lengths {lengths}")
+    _run(wl, p, lengths)
+
+
+def test_prefill_short_prompts_and_window_longer_than_prompt():
+    wl = synth.small(GQA, sink=8, recent=16, topk=20, obs_window=32)
+    p = params_of(wl)
+    lengths = [20, 24, 25, 31, 45, 2]
+    _announce(f"snap_prefill short prompts (L <= sink+recent, L < w): lengths {lengths}")
+    _run(wl, p, lengths)
+
+
+def test_prefill_streaming_only():
+    wl = synth.small(GQA, topk=0)
+    p = params_of(wl)
+    lengths = [900, 150]
+    _announce(f"snap_prefill with topk = 0 (sinks and ring only): lengths {lengths}")
+    q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, [0, 1], 2)
+    _check_attention(p, lengths, q, k, v, out)
+    op = oracle_params(p)
+    for b, L in enumerate(lengths):
+        assert int(cache.pos[b]) == L and int(cache.n_topk[b]) == 0
+        for g in range(p.n_kv_heads):
+            ek = oracle.assemble(L, p.sink, p.recent, 0, oracle.f64(k[b, g, :L]), np.zeros(0, np.int32))
+            assert np.array_equal(cache.k[b, g].double().cpu().numpy(), ek)
+
+
+def _sampled_rows(p, qc, kc, vc, out, L, rows, heads):
+    """Output rows of one sequence recomputed by the oracle one by one: row i
+    of head h needs q_{h,i} and the keys and values of positions 0..i only.
+    qc [Hq][L][dk], kc / vc [Hkv][L][d] fp64 on the host."""
+    op = oracle_params(p)
+    G = op.group
+    worst = 0.0
+    for h in heads:
+        g = h // G
+        for i in rows:
+            qq = np.zeros((1, i + 1, p.d_qk))
+            qq[0, i] = qc[h, i]
+            exp = oracle.prefill_attn_group(op, i + 1, qq, kc[g, :i + 1], vc[g, :i + 1], rows=(i, i + 1))
+            got = out[h, i].double().cpu().numpy()
+            err = float(np.max(np.abs(got - exp[0, 0])))
+            worst = max(worst, err)
+            assert err <= TOL["bf16"], (h, i, err)
+    return worst
+
+
+def test_prefill_full_size_llama_32k():
+    """The one-layer 32k Llama shape at full size, in the launch bench.py
+    times: sampled output rows (first tiles, tile edges, the window, random)
+    of every head against the oracle one by one, every output row finite,
+    and the selection of three KV heads against the oracle's compression."""
+    wl = synth.WORKLOADS["llama8b-1layer-32k"]
+    p = params_of(wl)
+    L = wl.length
+    _announce(f"snap_prefill llama8b-1layer-32k at full size: L={L}, 32/8 heads")
+    dev = "cuda"
+    q, k, v = synth.prompt_batch(wl, 0, [L], device=dev)
+    cache = GpuCache(p, 1)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, 1, L))
+    out = torch.empty((1, p.n_q_heads, L, p.d_v), dtype=torch.bfloat16, device=dev)
+    sel = torch.empty((1, p.n_kv_heads, p.topk), dtype=torch.int32, device=dev)
+    pooled = torch.empty((1, p.n_kv_heads, L), dtype=torch.float32, device=dev)
+    one = torch.zeros(1, dtype=torch.int32, device=dev)
+    lens = torch.tensor([L], dtype=torch.int32, device=dev)
+    snap.snap_prefill(p, cache.c(), cache.pos, cache.n_topk, one, lens, q, k, v, out, ws, sel, pooled)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
+    gen = np.random.default_rng(5)
+    rows = sorted(set([0, 1, 63, 64, 65, 127, 4095, 4096] + list(range(L - 33, L)) +
+                      gen.integers(0, L, 6).tolist()))
+    qc, kc, vc = oracle.f64(q[0]), oracle.f64(k[0]), oracle.f64(v[0])
+    err = _sampled_rows(p, qc, kc, vc, out[0], L, rows[::3], range(p.n_q_heads))
+    err = max(err, _sampled_rows(p, qc, kc, vc, out[0], L, rows, [0, 13, 31]))
+    op = oracle_params(p)
+    qobs = oracle.window_queries(op, [L], qc[None])
+    G = op.group
+    worst = 0.0
+    for g in [0, 3, 7]:
+        res = oracle.compress_group(op, L, qobs[0, g * G:(g + 1) * G], kc[g], vc[g])
+        gs = sel[0, g].cpu().numpy()
+        swaps = check_selection(gs, res.P, L, p.sink, p.recent, p.topk)
+        gp = pooled[0, g, p.sink:L - p.recent].double().cpu().numpy()
+        P = res.P[p.sink:L - p.recent]
+        keff = min(L - p.sink - p.recent, p.topk)
+        tau = np.sort(P)[::-1][keff - 1]
+        band = (P >= tau / 4) & (P <= 4 * tau)
+        rel = float((np.abs(gp - P) / np.maximum(P, 1e-30))[band].max())
+        worst = max(worst, rel)
+        ek = oracle.assemble(L, p.sink, p.recent, p.topk, kc[g], gs[:keff])
+        assert np.array_equal(cache.k[0, g].double().cpu().numpy(), ek)
+        print(f"  head {g}: swaps {swaps}, band rel err {rel:.3e}", flush=True)
+    print(f"  sampled attention max abs err {err:.3e}", flush=True)
+    assert worst <= BAND_RTOL
+    assert int(cache.pos[0]) == L and int(cache.n_topk[0]) == p.topk

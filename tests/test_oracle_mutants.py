@@ -69,8 +69,10 @@ MUTANTS = [
      "oi[d] += e * v[(size_t)j * dv + (d ^ 1)];"),
     ("prefill query rows read position-major", "const double* qi = q + ((size_t)h * L + i) * dk;",
      "const double* qi = q + ((size_t)i * G + h) * dk;"),
-    ("prefill normaliser without the row max", "lse[(size_t)h * L + i] = m + log(Z);",
-     "lse[(size_t)h * L + i] = log(Z);"),
+    ("prefill normaliser without the row max", "lse[(size_t)h * n + (i - i0)] = m + log(Z);",
+     "lse[(size_t)h * n + (i - i0)] = log(Z);"),
+    ("prefill rows of a range written one row late", "double* oi = out + ((size_t)h * n + (i - i0)) * dv;",
+     "double* oi = out + ((size_t)h * n + (i - i0 + (i0 > 0 && i + 1 < i1))) * dv;"),
     ("fp8 data scale from the largest positive value, not magnitude", "double a = fabs(x[i]);\n    if (a > amax)",
      "double a = x[i];\n    if (a > amax)"),
     ("fp8 data scale for the wrong top code", "return af / 448.0f;", "return af / 240.0f;"),

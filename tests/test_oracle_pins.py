@@ -580,3 +580,17 @@ def test_window_queries_are_the_last_w_positions():
     assert np.array_equal(got[0], q[0, :, 5:9])
     got = oracle.window_queries(p, [2], q)
     assert np.array_equal(got[0, :, 2:], q[0, :, 0:2]) and not got[0, :, :2].any()
+
+
+def test_prefill_row_range_matches_whole_prompt():
+    """A range of query rows (as the full-size tests sample them) equals the
+    same rows of the whole-prompt attention, against the library routine."""
+    p, q, k, v = _prefill_case(L=41)
+    G, L = q.shape[0], q.shape[1]
+    qt, kt, vt = (torch.from_numpy(x) for x in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        qt[None], kt[None, None].expand(1, G, L, -1), vt[None, None].expand(1, G, L, -1), is_causal=True,
+        scale=p.sm_scale)[0].numpy()
+    for i0, i1 in [(0, 1), (5, 9), (17, 41), (40, 41)]:
+        out = oracle.prefill_attn_group(p, L, q, k, v, rows=(i0, i1))
+        np.testing.assert_allclose(out, ref[:, i0:i1], rtol=1e-12, atol=1e-12)
