@@ -12,6 +12,14 @@ Prints ONE JSON line.  `value` is decoded tokens per second of the whole step
 (compression included); the decode-only rate, the per-layer decode-step HBM
 GB/s and the per-(sequence, layer) snap_compress latency are reported beside
 it.
+
+--prefill measures the other end of the path instead: one step is one
+snap_prefill call per layer (causal attention over every prompt position,
+then the compression with the window statistics taken from the attention
+pass).  `value` is prompt tokens per second per layer; the roofline is the
+attention kernel's bf16 MFMA rate, timed through snap_prefill_attn (the same
+attention without the compression), and the cost of the fused compression is
+reported beside the unfused snap_compress on the same window queries.
 """
 from __future__ import annotations
 
@@ -23,31 +31,39 @@ import sys
 import time
 
 DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
+DEFAULT_PREFILL_WORKLOAD = "llama8b-1layer-32k"
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
-    """sha256 of the gfx950 code object, in a built library's .hip_fatbin
-    section, that defines `symbol` (by default the decode kernels' object,
-    which also holds the combine): it changes when one of that object's kernels
-    changes, and not when only comments or the other objects' kernels do."""
-    import hashlib
+def _elf_section(d: bytes, want: bytes):
+    """Contents of the section named `want` of a 64-bit ELF image, or None."""
     import struct
-    try:
-        d = open(lib_path, "rb").read()
-    except OSError:
-        return None
     if d[:5] != b"\x7fELF\x02":
         return None
     shoff = struct.unpack_from("<Q", d, 0x28)[0]
     shentsize, shnum, shstrndx = struct.unpack_from("<HHH", d, 0x3A)
     sh = lambda i: struct.unpack_from("<IIQQQQ", d, shoff + i * shentsize)  # noqa: E731
     stroff = sh(shstrndx)[4]
-    fat = None
     for i in range(shnum):
         name, _, _, _, off, size = sh(i)
-        if d[stroff + name:d.index(b"\0", stroff + name)] == b".hip_fatbin":
-            fat = d[off:off + size]
+        if d[stroff + name:d.index(b"\0", stroff + name)] == want:
+            return d[off:off + size]
+    return None
+
+
+def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
+    """sha256 of the machine code (the .text section) of the gfx950 code
+    object, in a built library's .hip_fatbin section, that defines `symbol`
+    (by default the decode kernels' object, which also holds the combine): it
+    changes when one of that object's kernels changes, and not when only
+    comments, host code or the other objects' kernels do."""
+    import hashlib
+    import struct
+    try:
+        d = open(lib_path, "rb").read()
+    except OSError:
+        return None
+    fat = _elf_section(d, b".hip_fatbin")
     if fat is None:
         return None
     # offload bundles: magic, entry count, then (offset, size, triple length,
@@ -63,20 +79,25 @@ def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
             o += 24 + tl
             code = fat[b + off:b + off + size]
             if triple.endswith(b"gfx950") and symbol in code:
-                return hashlib.sha256(code).hexdigest()
+                text = _elf_section(code, b".text")
+                return None if text is None else hashlib.sha256(text).hexdigest()
         b = fat.find(magic, b + 1)
     return None
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per decode-step call from the committed counter runs
-    (profiles/traffic.json), or None when no record exists or the decode
-    kernels' code object has changed since the counters were taken."""
+PREFILL_SYMBOL = b"_ZN4snap12prefill_attnILi4EEEvNS_11PrefillArgsE"
+
+
+def measured_traffic(workload: str, symbol: bytes = b"_ZN4snap7combineE"):
+    """HBM bytes per launch of the roofline kernel from the committed counter
+    runs (profiles/traffic.json, keyed by workload; the prefill attention's
+    records by "prefill:" + workload), or None when no record exists or the
+    kernel's code object has changed since the counters were taken."""
     try:
         rec = json.load(open(os.path.join(HERE, "profiles", "traffic.json")))[workload]
     except (OSError, KeyError, ValueError):
         return None
-    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"))
+    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"), symbol)
     if code is None or code != rec.get("device_code_sha256"):
         return None
     return rec["traffic_bytes_per_launch"]
@@ -104,7 +125,9 @@ def parse():
                     help="timed steps (default 3; 64 for the continuous-batching workload)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps first (default 1; 32 for the continuous-batching workload)")
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--prefill", action="store_true",
+                    help="time snap_prefill (prefill attention + fused compression) instead of the decode step")
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (profiling only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -133,7 +156,11 @@ def main():
     import paper_2511_03092_amd as snap
     import synth
 
+    if args.workload is None:
+        args.workload = DEFAULT_PREFILL_WORKLOAD if args.prefill else DEFAULT_WORKLOAD
     wl = synth.WORKLOADS[args.workload]
+    if args.prefill:
+        return run_prefill(args, wl)
     if wl.slots is not None:
         return run_cb(args, wl)
     if args.steps is None:
@@ -511,6 +538,203 @@ def run_cb(args, wl):
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, p, timed_lengths, nd, layers, K, nd * K, value)
     print(json.dumps(res), flush=True)
+
+
+def run_prefill(args, wl):
+    """snap_prefill of one batch of prompts per layer (every sequence of the
+    workload, its lengths), prompts resident in HBM."""
+    import torch
+
+    import paper_2511_03092_amd as snap
+    import synth
+
+    if wl.in_dtype != "bf16" or wl.v_in_k:
+        sys.exit(f"--prefill needs a bf16 workload with separate K and V (got {wl.name})")
+    layers = args.layers or 1
+    n = wl.batch if wl.slots is None else 8
+    lengths = synth.draw_lengths(wl, 0, n)
+    max_len = max(lengths)
+    if args.steps is None:
+        args.steps = 10 if max_len * n <= 65536 else 2
+    if args.warmup is None:
+        args.warmup = 2 if max_len * n <= 65536 else 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
+    p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
+                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype])
+    kvt = {"bf16": torch.bfloat16, "fp8": torch.uint8}[wl.kv_dtype]
+    B = p.budget
+    t_setup = time.time()
+    prompts, caches = [], []
+    for l in range(layers):
+        prompts.append(synth.prompt_batch(wl, l, lengths, device=dev, max_len=max_len))
+        ck = torch.zeros((n, wl.n_kv_heads, B, wl.d_qk), dtype=kvt, device=dev)
+        cv = torch.zeros((n, wl.n_kv_heads, B, wl.d_v), dtype=kvt, device=dev)
+        ks = vs = None
+        if wl.kv_dtype == "fp8":
+            k_, v_ = prompts[-1][1], prompts[-1][2]
+            ks = torch.stack([k_[b, :, :lengths[b]].float().abs().amax(dim=(1, 2)) for b in range(n)]) / 448.0
+            vs = torch.stack([v_[b, :, :lengths[b]].float().abs().amax(dim=(1, 2)) for b in range(n)]) / 448.0
+            ks, vs = ks.clamp_min(1e-12).contiguous(), vs.clamp_min(1e-12).contiguous()
+        caches.append((ck, cv, ks, vs, snap.cache_struct(ck, cv, ks, vs)))
+    # the window queries for the unfused comparison (snap_compress), gathered untimed
+    qobs = []
+    for l in range(layers):
+        q = prompts[l][0]
+        qo = torch.zeros((n, wl.n_q_heads, wl.obs_window, wl.d_qk), dtype=q.dtype, device=dev)
+        for b, L in enumerate(lengths):
+            w = min(wl.obs_window, L)
+            qo[b, :, wl.obs_window - w:] = q[b, :, L - w:L]
+        qobs.append(qo)
+    pos = torch.zeros((n,), dtype=torch.int32, device=dev)
+    ntop = torch.zeros((n,), dtype=torch.int32, device=dev)
+    slots = torch.arange(n, dtype=torch.int32, device=dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, n, max_len), dev)
+    wsc = snap.workspace(snap.snap_compress_workspace(p, n, max_len), dev)
+    out = torch.empty((n, wl.n_q_heads, max_len, wl.d_v), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    if args.copy_calibration:
+        copy_calibration(torch, args.copy_calibration, dev)
+
+    def fused():
+        for l in range(layers):
+            q, k, v = prompts[l]
+            snap.snap_prefill(p, caches[l][4], pos, ntop, slots, lens, q, k, v, out, ws, stream=sptr)
+
+    def attn_only():
+        for l in range(layers):
+            q, k, v = prompts[l]
+            snap.snap_prefill_attn(p, lens, q, k, v, out, ws, stream=sptr)
+
+    def unfused_compress():
+        for l in range(layers):
+            _, k, v = prompts[l]
+            snap.snap_compress(p, caches[l][4], pos, ntop, slots, lens, qobs[l], k, v, wsc, stream=sptr)
+
+    for _ in range(args.warmup):
+        fused()
+        attn_only()
+        unfused_compress()
+    torch.cuda.synchronize()
+    # the three are interleaved step by step (clock drift over the run falls
+    # on all three alike); events bracket whole calls only
+    evs = []
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        fused()          # the reported step: snap_prefill, every layer
+        e[1].record(stream)
+        attn_only()      # the attention launch alone
+        e[2].record(stream)
+        unfused_compress()
+        e[3].record(stream)
+        evs.append(e)
+    torch.cuda.synchronize()
+    ms_step = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    ms_attn = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps / layers
+    ms_comp = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps / layers
+    ms_layer = ms_step / layers
+    tokens = sum(lengths)
+    # algorithmic flops of the causal attention: per row i, (i+1) keys x (2*d_qk + 2*d_v)
+    flop = sum(wl.n_q_heads * L * (L + 1) / 2 * (2 * wl.d_qk + 2 * wl.d_v) for L in lengths)
+    tflops = flop / (ms_attn * 1e-3) / 1e12
+    value = tokens * layers / (ms_step * 1e-3) / layers
+    res = {
+        "metric": "prefill attention + SnapKV compression (snap_prefill): prompt tok/s per layer",
+        "value": round(value, 1),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "launch": "eager",
+        "config": {"workload": wl.name, "layers": layers, "sequences": n, "prompt_lengths": lengths,
+                   "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
+                   "sink": wl.sink, "recent": wl.recent, "topk": wl.topk, "obs_window": wl.obs_window,
+                   "pool_kernel": wl.pool_kernel, "kv_dtype": wl.kv_dtype},
+        "prefill_ms_per_layer_call": round(ms_layer, 4),
+        "attention_ms_per_layer_call": round(ms_attn, 4),
+        "fused_compress_ms_per_layer_call": round(ms_layer - ms_attn, 4),
+        "fused_compress_frac_of_prefill": round((ms_layer - ms_attn) / ms_layer, 5),
+        "unfused_compress_ms_per_layer_call": round(ms_comp, 4),
+        "roofline": {"bound": "mfma", "kernel": "prefill_attn (+ vt_transpose), timed as snap_prefill_attn",
+                     "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("prefill:" + wl.name, PREFILL_SYMBOL),
+                     "algorithmic_flops_per_launch": flop},
+        "setup_s": round(t_setup, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_prefill(wl, p, lengths, layers, value)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
+    """The fp64 oracle's causal attention on the host's cores, on a bounded
+    sample: the last rows of one query head at the longest prompt (each row
+    needs all of its keys), rows added until about budget_s of one-thread
+    work; then the same rows of T heads on T threads at once.  Extrapolated
+    by flops to the attention of every head and position of every prompt and
+    layer; `value` is the T-thread rate in prompt tokens per second per
+    layer."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+    import synth
+
+    T = max(1, min(os.cpu_count() or 1, 16))
+    op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
+                       p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
+    L = max(lengths)
+    q, k, v = synth.prompt_batch(wl, 0, [L], device="cpu")
+    kc, vc = oracle.f64(k[0, 0]), oracle.f64(v[0, 0])
+    qh = [oracle.f64(q[0, h]) for h in range(min(T, p.n_q_heads))]
+
+    def rows(h, i0, i1):
+        qq = np.zeros((1, L, p.d_qk))
+        qq[0, i0:i1] = qh[h % len(qh)][i0:i1]
+        oracle.prefill_attn_group(op, L, qq, kc, vc, rows=(i0, i1))
+
+    nrow, t1 = 8, 0.0
+    while True:
+        t = time.time()
+        rows(0, L - nrow, L)
+        t1 = time.time() - t
+        if t1 >= budget_s / 4 or nrow >= L:
+            break
+        nrow = min(L, nrow * 4)
+    with ThreadPoolExecutor(T) as ex:
+        t = time.time()
+        list(ex.map(lambda h: rows(h, L - nrow, L), range(T)))
+        tT = time.time() - t
+    macs_row = lambda i: (i + 1) * (p.d_qk + p.d_v)
+    sample_macs = sum(macs_row(i) for i in range(L - nrow, L))
+    total_macs = sum(p.n_q_heads * Lb * (Lb + 1) / 2 * (p.d_qk + p.d_v) for Lb in lengths)
+    rate1 = sample_macs / t1
+    rateT = T * sample_macs / tT
+    tokens = sum(lengths)
+    val1 = tokens / (total_macs / rate1)
+    valT = tokens / (total_macs / rateT)
+    return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
+            "single_thread_value": float(f"{val1:.6g}"),
+            "sample": (f"causal attention rows {L - nrow}..{L - 1} of one head at L={L} (fp64 oracle): "
+                       f"{t1:.2f} s on one thread, the same rows of {T} heads on {T} threads in {tT:.2f} s; "
+                       f"extrapolated by multiply-adds to every head and position of {len(lengths)} prompt(s), "
+                       f"per layer (the compression's oracle cost is not included)"),
+            "gpu_over_cpu": float(f"{gpu_value / valT:.4g}")}
 
 
 def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_value, dec_budget_s=1.0):

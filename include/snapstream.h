@@ -187,6 +187,15 @@ snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t*
                          const void* q, const void* k, const void* v, void* out, int32_t* sel_out,
                          float* pooled_out, void* workspace, size_t ws_bytes, void* stream);
 
+/* The attention step of snap_prefill alone (Sec. IV-A): out as in
+ * snap_prefill, no cache or metadata written, no selection.  For layers that
+ * are not compressed, and for timing the attention apart from the
+ * compression.  Same supported shapes, workspace (snap_prefill_workspace) and
+ * errors as snap_prefill. */
+snap_status snap_prefill_attn(const snap_params* p, int32_t n_seq, const int32_t* lengths, int32_t max_len,
+                              const void* q, const void* k, const void* v, void* out, void* workspace,
+                              size_t ws_bytes, void* stream);
+
 /* Decode KV update (Sec. III-C): for each of the n sequences, the new token's
  * keys/values k_new [n][n_kv_heads][d_qk] and v_new [n][n_kv_heads][d_v]
  * (in_dtype; v_new NULL when v_in_k) are written to row

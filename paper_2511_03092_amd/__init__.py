@@ -6,7 +6,7 @@ used for device memory and the current stream.  If the library is missing the
 first call raises -- there is no other implementation behind these names.
 
 Functions keep the C names (include/snapstream.h):
-    snap_compress, snap_prefill, snap_cache_append, snap_decode_attn, snap_decode_step, snap_advance,
+    snap_compress, snap_prefill, snap_prefill_attn, snap_cache_append, snap_decode_attn, snap_decode_step, snap_advance,
     snap_compress_workspace, snap_prefill_workspace, snap_decode_workspace, snap_status_str
 """
 from __future__ import annotations
@@ -25,7 +25,7 @@ SNAP_NORM_CAND, SNAP_NORM_ROW = 0, 1
 SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
 
 EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_prefill_workspace", "snap_compress",
-            "snap_prefill", "snap_cache_append",
+            "snap_prefill", "snap_prefill_attn", "snap_cache_append",
             "snap_decode_attn", "snap_decode_step", "snap_advance", "snap_status_str", "snap_last_error"]
 
 
@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.snap_prefill_workspace.restype = sz
     L.snap_prefill.argtypes = [P, C, vp, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.snap_prefill.restype = ctypes.c_int
+    L.snap_prefill_attn.argtypes = [P, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.snap_prefill_attn.restype = ctypes.c_int
     L.snap_cache_append.argtypes = [P, C, vp, i32, vp, vp, vp, vp]
     L.snap_cache_append.restype = ctypes.c_int
     L.snap_decode_attn.argtypes = [P, C, vp, vp, i32, vp, vp, vp, i32, vp, sz, vp]
@@ -170,6 +172,13 @@ def snap_prefill(p: Params, cache: SnapCache, pos, n_topk, slot_ids, lengths, q,
                               _ptr(slot_ids), _ptr(lengths), max_len, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                               _ptr(sel_out), _ptr(pooled_out), _ptr(workspace),
                               workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def snap_prefill_attn(p: Params, lengths, q, k, v, out, workspace, stream=None):
+    n_seq, max_len = int(k.shape[0]), int(k.shape[2])
+    _check(lib().snap_prefill_attn(ctypes.byref(p.c()), n_seq, _ptr(lengths), max_len, _ptr(q), _ptr(k), _ptr(v),
+                                   _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                   _stream(stream)))
 
 
 def snap_cache_append(p: Params, cache: SnapCache, pos, slot_ids, k_new, v_new=None, stream=None):

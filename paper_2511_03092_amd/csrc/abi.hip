@@ -143,14 +143,10 @@ size_t snap_prefill_workspace(const snap_params* p, int32_t n_seq, int32_t max_l
   return prefill_geometry(*p, n_seq, max_len).prefill_bytes;
 }
 
-snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t* pos, int32_t* n_topk, int32_t n_seq,
-                         const int32_t* slot_ids, const int32_t* lengths, int32_t max_len, const void* q, const void* k,
-                         const void* v, void* out, int32_t* sel_out, float* pooled_out, void* workspace,
-                         size_t ws_bytes, void* stream) {
-  g_err[0] = 0;
-  snap_status st = check_params(p);
-  if (st != SNAP_OK) return st;
-  if ((st = check_cache(p, cache)) != SNAP_OK) return st;
+// Checks shared by snap_prefill and snap_prefill_attn.
+static snap_status check_prefill(const snap_params* p, int32_t n_seq, const int32_t* lengths, int32_t max_len,
+                                 const void* q, const void* k, const void* v, void* out, void* workspace,
+                                 size_t ws_bytes) {
   if (p->in_dtype != SNAP_BF16) return fail(SNAP_ERR_UNSUPPORTED, "snap_prefill takes bf16 inputs");
   if (p->v_in_k || p->d_qk != p->d_v || (p->d_qk != 64 && p->d_qk != 128))
     return fail(SNAP_ERR_UNSUPPORTED, "snap_prefill supports d_qk == d_v in {64, 128} with a separate V");
@@ -160,15 +156,42 @@ snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t*
   if (n_seq < 0) return fail(SNAP_ERR_INVALID_ARG, "n_seq must be >= 0");
   if (n_seq == 0) return SNAP_OK;
   if (max_len < 1 || max_len > (1 << 28)) return fail(SNAP_ERR_INVALID_ARG, "max_len must be in [1, 2^28]");
-  if (!pos || !n_topk || !slot_ids || !lengths) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids/lengths NULL");
+  if (!lengths) return fail(SNAP_ERR_INVALID_ARG, "lengths is NULL");
   if (!q || !aligned16(q) || !k || !aligned16(k) || !v || !aligned16(v))
     return fail(SNAP_ERR_INVALID_ARG, "q, k and v must be non-NULL and 16-byte aligned");
   if (!out || !aligned16(out)) return fail(SNAP_ERR_INVALID_ARG, "out is NULL or not 16-byte aligned");
-  if ((sel_out && !aligned16(sel_out)) || (pooled_out && !aligned16(pooled_out)))
-    return fail(SNAP_ERR_INVALID_ARG, "sel_out/pooled_out must be 16-byte aligned");
   const size_t need = prefill_geometry(*p, n_seq, max_len).prefill_bytes;
   if (!workspace || ((uintptr_t)workspace & 255u) || ws_bytes < need)
     return fail(SNAP_ERR_WORKSPACE, "workspace needs %zu bytes, 256-byte aligned (got %zu)", need, ws_bytes);
+  return SNAP_OK;
+}
+
+snap_status snap_prefill_attn(const snap_params* p, int32_t n_seq, const int32_t* lengths, int32_t max_len,
+                              const void* q, const void* k, const void* v, void* out, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  snap_status st = check_params(p);
+  if (st != SNAP_OK) return st;
+  if ((st = check_prefill(p, n_seq, lengths, max_len, q, k, v, out, workspace, ws_bytes)) != SNAP_OK) return st;
+  if (n_seq == 0) return SNAP_OK;
+  st = launch_prefill_attn(*p, n_seq, lengths, max_len, q, k, v, out, false, workspace, (hipStream_t)stream);
+  if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return st;
+}
+
+snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t* pos, int32_t* n_topk, int32_t n_seq,
+                         const int32_t* slot_ids, const int32_t* lengths, int32_t max_len, const void* q, const void* k,
+                         const void* v, void* out, int32_t* sel_out, float* pooled_out, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  snap_status st = check_params(p);
+  if (st != SNAP_OK) return st;
+  if ((st = check_cache(p, cache)) != SNAP_OK) return st;
+  if ((st = check_prefill(p, n_seq, lengths, max_len, q, k, v, out, workspace, ws_bytes)) != SNAP_OK) return st;
+  if (n_seq == 0) return SNAP_OK;
+  if (!pos || !n_topk || !slot_ids) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids NULL");
+  if ((sel_out && !aligned16(sel_out)) || (pooled_out && !aligned16(pooled_out)))
+    return fail(SNAP_ERR_INVALID_ARG, "sel_out/pooled_out must be 16-byte aligned");
   st = launch_prefill(*p, *cache, pos, n_topk, n_seq, slot_ids, lengths, max_len, q, k, v, out, sel_out, pooled_out,
                       workspace, (hipStream_t)stream);
   if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));

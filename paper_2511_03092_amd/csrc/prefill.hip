@@ -394,17 +394,15 @@ Geometry prefill_geometry(const snap_params& p, int n_seq, int max_len) {
   return g;
 }
 
-snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* pos, int32_t* n_topk, int n_seq,
-                           const int32_t* slot_ids, const int32_t* lengths, int max_len, const void* q, const void* k,
-                           const void* v, void* out, int32_t* sel_out, float* pooled_out, void* ws,
-                           hipStream_t stream) {
+snap_status launch_prefill_attn(const snap_params& p, int n_seq, const int32_t* lengths, int max_len, const void* q,
+                                const void* k, const void* v, void* out, bool want_stats, void* ws,
+                                hipStream_t stream) {
   const Geometry geo = prefill_geometry(p, n_seq, max_len);
   const int groups = n_seq * p.n_kv_heads;
   const int G = p.n_q_heads / p.n_kv_heads;
   const float scale = p.sm_scale > 0.f ? p.sm_scale : 1.0f / sqrtf((float)p.d_qk);
   unsigned char* w = (unsigned char*)ws;
   uint16_t* vt = (uint16_t*)(w + geo.off_vt);
-  const bool select = p.topk > 0 || pooled_out;
 
   dim3 tgrid(geo.ld_vt / 64, groups);
   if (p.d_qk == 128)
@@ -434,7 +432,7 @@ snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* p
   pa.norm = p.norm;
   pa.rows = geo.rows;
   pa.rows_pad = geo.rows_pad;
-  pa.want_stats = select ? 1 : 0;
+  pa.want_stats = want_stats ? 1 : 0;
   pa.P = prefill_positions(G);
   pa.scale2 = (float)((double)scale * 1.4426950408889634074);
   pa.n_qblocks = (max_len + pa.P - 1) / pa.P;
@@ -445,9 +443,19 @@ snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* p
   else
     hipLaunchKernelGGL(prefill_attn<2>, grid, dim3(256), 0, stream, pa);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
+  return SNAP_OK;
+}
 
-  return launch_compress(p, c, pos, n_topk, n_seq, slot_ids, lengths, max_len, pa.qobs, k, v, sel_out, pooled_out, ws,
-                         stream, /*stats_given=*/true);
+snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* pos, int32_t* n_topk, int n_seq,
+                           const int32_t* slot_ids, const int32_t* lengths, int max_len, const void* q, const void* k,
+                           const void* v, void* out, int32_t* sel_out, float* pooled_out, void* ws,
+                           hipStream_t stream) {
+  const bool select = p.topk > 0 || pooled_out;
+  snap_status st = launch_prefill_attn(p, n_seq, lengths, max_len, q, k, v, out, select, ws, stream);
+  if (st != SNAP_OK) return st;
+  const Geometry geo = prefill_geometry(p, n_seq, max_len);
+  return launch_compress(p, c, pos, n_topk, n_seq, slot_ids, lengths, max_len, (unsigned char*)ws + geo.off_qobs, k,
+                         v, sel_out, pooled_out, ws, stream, /*stats_given=*/true);
 }
 
 }  // namespace snap

@@ -146,6 +146,11 @@ snap_status launch_prefill(const snap_params& p, const snap_cache& c, int32_t* p
                            const int32_t* slot_ids, const int32_t* lengths, int max_len, const void* q, const void* k,
                            const void* v, void* out, int32_t* sel_out, float* pooled_out, void* ws,
                            hipStream_t stream);
+// the attention part of launch_prefill; want_stats: also the window rows'
+// statistics and queries (into the compress part of the workspace)
+snap_status launch_prefill_attn(const snap_params& p, int n_seq, const int32_t* lengths, int max_len, const void* q,
+                                const void* k, const void* v, void* out, bool want_stats, void* ws,
+                                hipStream_t stream);
 snap_status launch_append(const snap_params& p, const snap_cache& c, const int32_t* pos, int n,
                           const int32_t* slot_ids, const void* k_new, const void* v_new,
                           hipStream_t stream);

@@ -195,3 +195,20 @@ def test_prefill_validation():
                           None, FAKE, None, None, FAKE, 1 << 34, None) == snap.SNAP_ERR_UNSUPPORTED
     # a supported fp8 cache still needs its scales
     assert pre(params=_params(kv_dtype=snap.SNAP_FP8_E4M3)) == snap.SNAP_ERR_INVALID_ARG
+
+
+def test_prefill_attn_validation():
+    L = snap.lib()
+    p = _params()
+
+    def att(params=p, q=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 34, n_seq=1, max_len=4096, lengths=FAKE):
+        return L.snap_prefill_attn(ctypes.byref(params.c()), n_seq, lengths, max_len, q, k, v, out, ws, ws_bytes, None)
+
+    need = snap.snap_prefill_workspace(p, 1, 4096)
+    assert att(out=None) == snap.SNAP_ERR_INVALID_ARG
+    assert att(lengths=None) == snap.SNAP_ERR_INVALID_ARG
+    assert att(k=FAKE + 4) == snap.SNAP_ERR_INVALID_ARG
+    assert att(ws_bytes=need - 1) == snap.SNAP_ERR_WORKSPACE
+    assert att(n_seq=0) == snap.SNAP_OK
+    assert att(params=_params(d_qk=576, d_v=512, v_in_k=1, n_q_heads=8, n_kv_heads=1)) == snap.SNAP_ERR_UNSUPPORTED
+    assert att(params=_params(pool_kernel=2)) == snap.SNAP_ERR_INVALID_ARG

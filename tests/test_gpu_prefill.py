@@ -184,3 +184,22 @@ def test_prefill_full_size_llama_32k():
     print(f"  sampled attention max abs err {err:.3e}", flush=True)
     assert worst <= BAND_RTOL
     assert int(cache.pos[0]) == L and int(cache.n_topk[0]) == p.topk
+
+
+def test_prefill_attn_alone_matches_prefill_output():
+    """snap_prefill_attn runs the same attention without the compression: its
+    output equals snap_prefill's bit for bit and matches the oracle."""
+    wl = GQA
+    p = params_of(wl)
+    lengths = [1000, 333, 97, 1]
+    _announce(f"snap_prefill_attn alone vs snap_prefill: lengths {lengths}")
+    q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, [0, 1, 2, 3], 4)
+    dev = "cuda"
+    n, ml = k.shape[0], k.shape[2]
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    out2 = torch.full_like(out, float("nan"))
+    snap.snap_prefill_attn(p, lens, q.to(dev), k.to(dev), v.to(dev), out2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(out2.view(torch.int16), out.view(torch.int16))
+    _check_attention(p, lengths, q, k, v, out2)
