@@ -51,12 +51,38 @@ def _elf_section(d: bytes, want: bytes):
     return None
 
 
-def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
-    """sha256 of the machine code (the .text section) of the gfx950 code
-    object, in a built library's .hip_fatbin section, that defines `symbol`
-    (by default the decode kernels' object, which also holds the combine): it
-    changes when one of that object's kernels changes, and not when only
-    comments, host code or the other objects' kernels do."""
+def _kernel_code(code: bytes, pattern: str):
+    """Machine code of the functions of an ELF code object whose symbol names
+    match `pattern` (a regular expression), concatenated in name order."""
+    import re
+    import struct
+    if code[:5] != b"\x7fELF\x02":
+        return None
+    shoff = struct.unpack_from("<Q", code, 0x28)[0]
+    shentsize, shnum = struct.unpack_from("<HH", code, 0x3A)
+    secs = [struct.unpack_from("<IIQQQQIIQQ", code, shoff + i * shentsize) for i in range(shnum)]
+    out = []
+    for _, type_, _, _, off, size, link, _, _, entsize in secs:
+        if type_ != 2:  # SHT_SYMTAB
+            continue
+        stroff = secs[link][4]
+        for j in range(size // entsize):
+            st_name, st_info, _, st_shndx, st_value, st_size = struct.unpack_from("<IBBHQQ", code, off + j * entsize)
+            nm = code[stroff + st_name:code.index(b"\0", stroff + st_name)].decode()
+            if (st_info & 0xF) == 2 and st_size and re.search(pattern, nm):  # STT_FUNC
+                sec = secs[st_shndx]
+                start = sec[4] + (st_value - sec[3])
+                out.append((nm, code[start:start + st_size]))
+    if not out:
+        return None
+    return b"".join(c for _, c in sorted(out))
+
+
+def device_code_sha256(lib_path: str, kernels: str):
+    """sha256 of the machine code of the kernels whose symbol names match
+    `kernels` (a regular expression), in the gfx950 code objects of a built
+    library's .hip_fatbin section: it changes when one of those kernels
+    changes, and not when only comments, host code or other kernels do."""
     import hashlib
     import struct
     try:
@@ -69,6 +95,7 @@ def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
     # offload bundles: magic, entry count, then (offset, size, triple length,
     # triple) per entry, offsets from the bundle's start
     magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    parts = []
     b = fat.find(magic)
     while b >= 0:
         n = struct.unpack_from("<Q", fat, b + len(magic))[0]
@@ -77,27 +104,25 @@ def device_code_sha256(lib_path: str, symbol: bytes = b"_ZN4snap7combineE"):
             off, size, tl = struct.unpack_from("<QQQ", fat, o)
             triple = fat[o + 24:o + 24 + tl]
             o += 24 + tl
-            code = fat[b + off:b + off + size]
-            if triple.endswith(b"gfx950") and symbol in code:
-                text = _elf_section(code, b".text")
-                return None if text is None else hashlib.sha256(text).hexdigest()
+            if triple.endswith(b"gfx950"):
+                k = _kernel_code(fat[b + off:b + off + size], kernels)
+                if k:
+                    parts.append(k)
         b = fat.find(magic, b + 1)
-    return None
+    return hashlib.sha256(b"".join(parts)).hexdigest() if parts else None
 
 
-PREFILL_SYMBOL = b"_ZN4snap12prefill_attnILi4EEEvNS_11PrefillArgsE"
-
-
-def measured_traffic(workload: str, symbol: bytes = b"_ZN4snap7combineE"):
+def measured_traffic(workload: str):
     """HBM bytes per launch of the roofline kernel from the committed counter
     runs (profiles/traffic.json, keyed by workload; the prefill attention's
     records by "prefill:" + workload), or None when no record exists or the
-    kernel's code object has changed since the counters were taken."""
+    machine code of the record's kernels (its "kernels" pattern) has changed
+    since the counters were taken."""
     try:
         rec = json.load(open(os.path.join(HERE, "profiles", "traffic.json")))[workload]
     except (OSError, KeyError, ValueError):
         return None
-    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"), symbol)
+    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"), rec["kernels"])
     if code is None or code != rec.get("device_code_sha256"):
         return None
     return rec["traffic_bytes_per_launch"]
@@ -137,6 +162,9 @@ def parse():
                     help="run each step's decode phase as one captured HIP graph (replayed every step)")
     ap.add_argument("--fp8-scales-from-data", action="store_true",
                     help="continuous batching: snap_compress sets the fp8 scales (amax / 448 of the kept rows)")
+    ap.add_argument("--fp8-qk", action="store_true",
+                    help="fp8 caches: quantise each decode query head to E4M3 and run Q K^T on the fp8 MFMA "
+                         "(snap_params.fp8_qk)")
     ap.add_argument("--overlap", action="store_true",
                     help="continuous batching: run each step's compression and decode on two streams at once")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -370,7 +398,8 @@ def run_cb(args, wl):
     DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
     p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
                     wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype],
-                    fp8_scales=snap.SNAP_FP8_SCALES_AMAX if args.fp8_scales_from_data else snap.SNAP_FP8_SCALES_GIVEN)
+                    fp8_scales=snap.SNAP_FP8_SCALES_AMAX if args.fp8_scales_from_data else snap.SNAP_FP8_SCALES_GIVEN,
+                    fp8_qk=1 if args.fp8_qk else 0)
     B = p.budget
     Lmax = wl.max_len
     n_steps = args.warmup + args.steps
@@ -519,7 +548,8 @@ def run_cb(args, wl):
                    "step": "compress one new prompt into the retired slot (every layer), then one decode "
                            "step of the other slots",
                    "fp8_scales": "amax/448 of the kept rows, set by snap_compress" if args.fp8_scales_from_data
-                   else "amax/448 of the layer's prompt bank, set by the harness"},
+                   else "amax/448 of the layer's prompt bank, set by the harness",
+                   "fp8_qk": bool(args.fp8_qk)},
         "decode_step_ms_per_call": round(dec_ms, 4),
         "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(nd / (dec_ms * layers * 1e-3), 1) if dec_ms > 0 else 0.0,
@@ -529,9 +559,11 @@ def run_cb(args, wl):
                        "tflops_over_compress_call": round(score_tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
                        "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4)},
         "roofline": {"bound": "hbm",
-                     "kernel": "snap_decode_step (fp8 cache: append + split-K attention, one launch) + combine",
+                     "kernel": "snap_decode_step (fp8 cache: append + split-K attention, one launch) + combine"
+                               + (", fp8 Q K^T" if args.fp8_qk else ""),
                      "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(wl.name),
+                     "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
+                     "traffic": None if args.fp8_qk else measured_traffic(wl.name),
                      "algorithmic_bytes_per_launch": round(dec_bytes_call)},
         "setup_s": round(t_setup, 1),
     }
@@ -671,7 +703,7 @@ def run_prefill(args, wl):
         "roofline": {"bound": "mfma", "kernel": "prefill_attn (+ vt_transpose), timed as snap_prefill_attn",
                      "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic("prefill:" + wl.name, PREFILL_SYMBOL),
+                     "traffic": measured_traffic("prefill:" + wl.name),
                      "algorithmic_flops_per_launch": flop},
         "setup_s": round(t_setup, 1),
     }

@@ -95,6 +95,16 @@ typedef struct {
                           same) or SNAP_FP8_E4M3 (with SNAP_BF16 inputs)          */
   float sm_scale;      /* softmax scale; <= 0 means 1/sqrt(d_qk)                 */
   int32_t fp8_scales;  /* snap_fp8_scales (fp8 caches; ignored otherwise)        */
+  int32_t fp8_qk;      /* decode attention over an fp8 cache: 0 = Q K^T in bf16
+                          (the codes converted exactly); 1 = the query of each
+                          head quantised to E4M3 with scale amax|q_h| / 448 (1
+                          when q_h is zero; codes round to nearest even on the
+                          fp32 quotient) and Q K^T on the fp8 MFMA.  Mode 1
+                          changes the logits by the query's quantisation error
+                          (about 2^-4 relative per element): it needs bf16
+                          inputs, a GQA fp8 cache, d_qk = d_v = 128
+                          (SNAP_ERR_UNSUPPORTED otherwise).  Values stay bf16
+                          products.                                              */
 } snap_params;
 
 /* One layer's compressed cache (device memory, caller-owned, row-major):

@@ -33,7 +33,8 @@ class SnapParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_q_heads", "n_kv_heads", "d_qk", "d_v", "v_in_k", "sink", "recent", "topk",
         "obs_window", "pool_kernel", "pool", "norm", "in_dtype", "kv_dtype")] + [("sm_scale", ctypes.c_float),
-                                                                                  ("fp8_scales", ctypes.c_int32)]
+                                                                                  ("fp8_scales", ctypes.c_int32),
+                                                                                  ("fp8_qk", ctypes.c_int32)]
 
 
 class SnapCache(ctypes.Structure):
@@ -108,6 +109,7 @@ class Params:
     kv_dtype: int = SNAP_BF16
     sm_scale: float = 0.0
     fp8_scales: int = SNAP_FP8_SCALES_GIVEN
+    fp8_qk: int = 0
 
     @property
     def budget(self) -> int:
@@ -116,7 +118,8 @@ class Params:
     def c(self) -> SnapParams:
         return SnapParams(self.n_q_heads, self.n_kv_heads, self.d_qk, self.d_v, int(self.v_in_k), self.sink,
                           self.recent, self.topk, self.obs_window, self.pool_kernel, self.pool, self.norm,
-                          self.in_dtype, self.kv_dtype, float(self.sm_scale), int(self.fp8_scales))
+                          self.in_dtype, self.kv_dtype, float(self.sm_scale), int(self.fp8_scales),
+                          int(self.fp8_qk))
 
 
 def _ptr(t) -> int | None:

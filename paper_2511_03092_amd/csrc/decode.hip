@@ -194,8 +194,11 @@ __device__ __forceinline__ void new_piece_store(const DecodeArgs& a, int g, int 
 // KSTEPS = dk / 32, VPASS = dv / 128.  Lane l owns head l%16 of the group and,
 // per 16-row set, the output rows 4*(l/16)+e; P never leaves the lane between
 // the two products because the V operand is loaded in the matching row order.
-template <int KSTEPS, int VPASS, bool FP8>
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+template <int KSTEPS, int VPASS, bool FP8, bool QK8 = false>
 __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
+  static_assert(!QK8 || (FP8 && KSTEPS == 4), "fp8 products need an fp8 cache of 128-wide rows");
   constexpr int D = KSTEPS * 32;
   typedef typename Raw8<FP8>::T RawT;
   const int lane = tid(), l16 = lane & 15, lg = lane >> 4;
@@ -222,7 +225,30 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   const size_t row0 = ((size_t)slot * a.Hkv + g) * (size_t)B;
   const float ksc = FP8 ? a.k_scale[(size_t)slot * a.Hkv + g] : 1.f;
   const float vsc = FP8 ? (a.cv ? a.v_scale : a.k_scale)[(size_t)slot * a.Hkv + g] : 1.f;
-  const float xs = a.scale * kLog2e * ksc;
+  // QK8: this lane's head (l16) quantised to E4M3 with scale amax|q| / 448
+  // (the lane holds dims 32*lg .. 32*lg+31, the fp8 MFMA's k-slots for them)
+  i32x8 q8 = {0, 0, 0, 0, 0, 0, 0, 0};
+  float qsc = 1.f;
+  if constexpr (QK8) {
+    float amax = 0.f;
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      const u32x4 w = __builtin_bit_cast(u32x4, qf[t]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        amax = fmaxf(amax, fmaxf(fabsf(bf16_bits_to_f32(w[i] & 0xffffu)), fabsf(bf16_bits_to_f32(w[i] >> 16))));
+    }
+    amax = fmaxf(amax, __shfl_xor(amax, 16));
+    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    qsc = amax > 0.f ? amax / 448.f : 1.f;
+#pragma unroll
+    for (int t = 0; t < KSTEPS; ++t) {
+      const u32x2 c = bf16x8_to_e4m3x8(__builtin_bit_cast(u32x4, qf[t]), qsc);
+      q8[2 * t] = (int)c[0];
+      q8[2 * t + 1] = (int)c[1];
+    }
+  }
+  const float xs = a.scale * kLog2e * ksc * qsc;
   const void* vbase = a.cv ? a.cv : a.ck;
   const int vstride = a.cv ? a.dv : a.dk;
   // fused append: row vnew comes from k_new / v_new (quantised for fp8 caches)
@@ -319,10 +345,25 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
     if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
 
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (QK8) {
+      // one fp8 MFMA per 16 rows: the lane's 32 codes of each row against the
+      // head's 32 query codes (E4M3 both, unit block scales)
+      i32x8 k8a, k8b;
 #pragma unroll
-    for (int t = 0; t < KSTEPS; ++t) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(ka[t])), qf[t], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(kb[t])), qf[t], s1, 0, 0, 0);
+      for (int t = 0; t < KSTEPS; ++t) {
+        k8a[2 * t] = (int)ka[t][0];
+        k8a[2 * t + 1] = (int)ka[t][1];
+        k8b[2 * t] = (int)kb[t][0];
+        k8b[2 * t + 1] = (int)kb[t][1];
+      }
+      s0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(k8a, q8, s0, 0, 0, 0, 127, 0, 127);
+      s1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(k8b, q8, s1, 0, 0, 0, 127, 0, 127);
+    } else {
+#pragma unroll
+      for (int t = 0; t < KSTEPS; ++t) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(ka[t])), qf[t], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf16x8_of<FP8>(kb[t])), qf[t], s1, 0, 0, 0);
+      }
     }
     // raw dot products; the scale (> 0, fp8 key scale included) is applied to
     // the block max and folded into the exponent
@@ -1132,7 +1173,9 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
       hipLaunchKernelGGL(decode_mla_lds, grid, dim3(256), 0, stream, a);
   } else if (mfma_ok) {
     dim3 grid(geo.n_chunks, n * p.n_kv_heads);
-    if (p.kv_dtype == SNAP_FP8_E4M3)
+    if (p.kv_dtype == SNAP_FP8_E4M3 && p.fp8_qk)
+      hipLaunchKernelGGL((decode_mfma<4, 1, true, true>), grid, dim3(64), 0, stream, a);
+    else if (p.kv_dtype == SNAP_FP8_E4M3)
       hipLaunchKernelGGL((decode_mfma<4, 1, true>), grid, dim3(64), 0, stream, a);
     else
       hipLaunchKernelGGL((decode_mfma<4, 1, false>), grid, dim3(64), 0, stream, a);

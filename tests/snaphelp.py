@@ -167,11 +167,25 @@ def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gse
     return dict(swaps=swaps, pooled_rel_err=rel, band_rel_err=band_rel, oracle=res)
 
 
+def fp8_query(q) -> np.ndarray:
+    """The decode query as fp8 products see it (snap_params.fp8_qk): each head
+    quantised to E4M3 with the oracle's data scale (amax / 448) and
+    dequantised exactly.  q [..., d] -> fp64 of the same shape."""
+    q = oracle.f64(q)
+    out = np.empty_like(q)
+    for idx in np.ndindex(q.shape[:-1]):
+        sc = oracle.fp8_scale(q[idx])
+        out[idx] = oracle.dequantize(oracle.quantize(q[idx], sc), sc)
+    return out
+
+
 def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, steps, out_dtype, tol,
-                 check_every=1, layer=0, salt=0, fused=False):
+                 check_every=1, layer=0, salt=0, fused=False, q_oracle=None, stats=None):
     """Run `steps` decode steps (append, attend, advance) and check each checked
     step against the oracle on the GPU's cache.  Returns the max abs error.
-    fused: append and attend through snap_decode_step instead of two calls."""
+    fused: append and attend through snap_decode_step instead of two calls.
+    q_oracle: the query the oracle attends with (e.g. fp8_query); stats, if a
+    dict, gets the max abs deviation from the oracle on the exact query."""
     dev = cache.k.device
     sl = torch.tensor(slots, dtype=torch.int32, device=dev)
     n = len(slots)
@@ -211,9 +225,13 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
                 for g in range(p.n_kv_heads):
                     codes = oracle.quantize(oracle.f64(kn[i, g]), float(cache.k_scale[s_, g]))
                     assert np.array_equal(cache.k[s_, g, row].cpu().numpy(), codes)
-        exp = oracle.decode_attn(op, positions, nt[slots], q, ck[slots], None if cv is None else cv[slots])
+        cvs = None if cv is None else cv[slots]
+        exp = oracle.decode_attn(op, positions, nt[slots], q if q_oracle is None else q_oracle(q), ck[slots], cvs)
         got = out.double().cpu().numpy()
         err = float(np.max(np.abs(got - exp)))
+        if stats is not None and q_oracle is not None:
+            exact = oracle.decode_attn(op, positions, nt[slots], q, ck[slots], cvs)
+            stats["exact_query_dev"] = max(stats.get("exact_query_dev", 0.0), float(np.max(np.abs(got - exact))))
         worst = max(worst, err)
         assert err <= tol, f"decode step {step}: max abs err {err}"
     return worst

@@ -212,3 +212,13 @@ def test_prefill_attn_validation():
     assert att(n_seq=0) == snap.SNAP_OK
     assert att(params=_params(d_qk=576, d_v=512, v_in_k=1, n_q_heads=8, n_kv_heads=1)) == snap.SNAP_ERR_UNSUPPORTED
     assert att(params=_params(pool_kernel=2)) == snap.SNAP_ERR_INVALID_ARG
+
+
+def test_fp8_qk_validation():
+    assert _compress_status(_params(fp8_qk=2))[0] == snap.SNAP_ERR_INVALID_ARG
+    assert _compress_status(_params(fp8_qk=1))[0] == snap.SNAP_ERR_UNSUPPORTED  # bf16 cache
+    assert _compress_status(_params(fp8_qk=1, kv_dtype=snap.SNAP_FP8_E4M3, d_qk=64, d_v=64))[0] == \
+        snap.SNAP_ERR_UNSUPPORTED
+    # a supported fp8 setting fails later (the fake cache has no scales), not on fp8_qk
+    st, msg = _compress_status(_params(fp8_qk=1, kv_dtype=snap.SNAP_FP8_E4M3))
+    assert st == snap.SNAP_ERR_INVALID_ARG and "scale" in msg

@@ -103,3 +103,28 @@ def test_step_fp8_fused_and_fp32_two_launch_paths():
     p = params_of(wl)
     _announce("decode_step fp32 tiny (generic kernel, two launches)")
     _fused_vs_two_calls(wl, p, [wl.length], [0], 1, 24, torch.float32)
+
+
+def test_fp8_query_products():
+    """snap_params.fp8_qk = 1 over a GQA fp8 cache: the query is quantised per
+    head and Q K^T runs on the fp8 MFMA.  Checked against the oracle attending
+    with the same quantised query (oracle.fp8_scale / quantize), to the fp8
+    tolerance; the deviation from the exact query is reported beside it.  The
+    fused step (new row quantised in LDS) and the two-call path both run."""
+    from snaphelp import fp8_query
+    wl = synth.small(GQA, kv_dtype="fp8")
+    p = params_of(wl, fp8_qk=1)
+    lengths = [2000, 900, 3]
+    _announce(f"fp8 query products (fp8_qk=1): lengths {lengths}, fused step then two calls")
+    q, k, v = synth.prefill_batch(wl, 0, lengths)
+    c = GpuCache(p, 3)
+    c.k_scale.fill_(0.05)
+    c.v_scale.fill_(0.05)
+    gpu_compress(p, c, q, k, v, lengths, [0, 1, 2], debug=False)
+    stats = {}
+    err = decode_steps(p, wl, c, [0, 1, 2], 6, torch.bfloat16, TOL["fp8"], salt=3, fused=True, q_oracle=fp8_query,
+                       stats=stats)
+    err2 = decode_steps(p, wl, c, [0, 1, 2], 3, torch.bfloat16, TOL["fp8"], salt=4, fused=False, q_oracle=fp8_query,
+                        stats=stats)
+    print(f"  max abs err vs oracle with the fp8 query: {max(err, err2):.3e}; "
+          f"deviation from the exact query: {stats['exact_query_dev']:.3e}", flush=True)
