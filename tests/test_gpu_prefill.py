@@ -203,3 +203,50 @@ def test_prefill_attn_alone_matches_prefill_output():
     torch.cuda.synchronize()
     assert torch.equal(out2.view(torch.int16), out.view(torch.int16))
     _check_attention(p, lengths, q, k, v, out2)
+
+
+@pytest.mark.parametrize("scales", ["given", "amax"])
+def test_prefill_into_fp8_cache(scales):
+    """snap_prefill into an fp8 cache: caller-set scales, or scales from the
+    kept rows (SNAP_FP8_SCALES_AMAX); every code against the oracle's
+    quantisation of the oracle's assembly, selection as for bf16."""
+    wl = synth.small(GQA, kv_dtype="fp8")
+    p = params_of(wl, fp8_scales=snap.SNAP_FP8_SCALES_AMAX if scales == "amax" else snap.SNAP_FP8_SCALES_GIVEN)
+    lengths = [1000, 333]
+    _announce(f"snap_prefill into an fp8 cache, scales {scales}: lengths {lengths}")
+    slots = [1, 0]
+    q, k, v = synth.prompt_batch(wl, 0, lengths, pad_value=float("nan"), slots=slots)
+    dev = "cuda"
+    n, ml = k.shape[0], k.shape[2]
+    cache = GpuCache(p, 2)
+    if scales == "given":
+        for b, s_ in enumerate(slots):
+            L = lengths[b]
+            cache.k_scale[s_] = k[b, :, :L].float().abs().amax(dim=(1, 2)).to(dev) / 448.0
+            cache.v_scale[s_] = v[b, :, :L].float().abs().amax(dim=(1, 2)).to(dev) / 448.0
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.tensor(slots, dtype=torch.int32, device=dev)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    out = torch.full((n, p.n_q_heads, ml, p.d_v), float("nan"), dtype=torch.bfloat16, device=dev)
+    sel = torch.empty((n, p.n_kv_heads, p.topk), dtype=torch.int32, device=dev)
+    pooled = torch.empty((n, p.n_kv_heads, ml), dtype=torch.float32, device=dev)
+    snap.snap_prefill(p, cache.c(), cache.pos, cache.n_topk, sl, lens, q.to(dev), k.to(dev), v.to(dev), out, ws,
+                      sel, pooled)
+    torch.cuda.synchronize()
+    _check_attention(p, lengths, q, k, v, out)
+    qobs = oracle.window_queries(oracle_params(p), lengths, q)
+    gsel = sel.cpu().numpy()
+    if scales == "amax":
+        # the scales the compression set: the oracle's data scale of the rows
+        # the cache keeps (for the selection the GPU made)
+        nt = cache.n_topk.cpu().numpy()
+        for b, s_ in enumerate(slots):
+            L = lengths[b]
+            for g in range(p.n_kv_heads):
+                used = gsel[b, g, :nt[s_]]
+                for src, sc in ((k, cache.k_scale), (v, cache.v_scale)):
+                    rows = oracle.assemble(L, p.sink, p.recent, p.topk, oracle.f64(src[b, g, :L]), used)
+                    assert float(sc[s_, g]) == oracle.fp8_scale(rows), (b, g)
+    st = check_compress(p, cache, qobs, k, v, lengths, slots, gsel, pooled.cpu().numpy())
+    print(f"  swaps {st['swaps']}, decision band {st['band_rel_err']:.3e}", flush=True)
+    assert st["band_rel_err"] <= BAND_RTOL
