@@ -9,7 +9,9 @@
  *   rows [sink+recent, B)          the top-K tokens chosen by SnapKV at the end
  *                                  of prefill (Sec. III-B.2, Eq. 1-3), followed
  *                                  by zeroed padding rows when fewer exist.
- * The library fills that cache from a padded prefill (snap_compress), writes
+ * The library fills that cache from a padded prefill (snap_compress; or
+ * snap_prefill, which also computes the prompt's causal attention and takes
+ * the window statistics from it), writes
  * each decoded token into its ring row (snap_cache_append, Sec. III-C), and
  * runs decode attention over the valid rows (snap_decode_attn; snap_decode_step
  * does both for one layer).
@@ -30,6 +32,10 @@
  *    [0, n_slots) makes the call skip that sequence.
  *  - Inputs must not alias the cache.  Calls on disjoint buffers may run
  *    concurrently on different streams.
+ *  - Batch limits of the launch grids: n_seq * n_kv_heads <= 65535
+ *    (snap_compress, snap_prefill, snap_prefill_attn) and n * n_q_heads <=
+ *    65535 (snap_decode_attn, snap_decode_step); larger calls return
+ *    SNAP_ERR_UNSUPPORTED (split the batch).
  */
 #ifndef SNAPSTREAM_H
 #define SNAPSTREAM_H

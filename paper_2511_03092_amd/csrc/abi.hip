@@ -29,6 +29,10 @@ static snap_status fail(snap_status s, const char* fmt, ...) {
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Largest second launch-grid dimension (workgroups along y): per-(sequence,
+// KV head) and per-(sequence, query head) grids must fit it.
+constexpr int kMaxGridY = 65535;
+
 // Parameter checks shared by every call.
 static snap_status check_params(const snap_params* p) {
   if (!p) return fail(SNAP_ERR_INVALID_ARG, "params is NULL");
@@ -126,6 +130,8 @@ snap_status snap_compress(const snap_params* p, const snap_cache* cache, int32_t
   if (n_seq < 0) return fail(SNAP_ERR_INVALID_ARG, "n_seq must be >= 0");
   if (n_seq == 0) return SNAP_OK;
   if (max_len < 1 || max_len > (1 << 28)) return fail(SNAP_ERR_INVALID_ARG, "max_len must be in [1, 2^28]");
+  if ((long long)n_seq * p->n_kv_heads > kMaxGridY)
+    return fail(SNAP_ERR_UNSUPPORTED, "n_seq * n_kv_heads must be at most %d", kMaxGridY);
   if (!pos || !n_topk || !slot_ids || !lengths) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids/lengths NULL");
   if (!q_obs || !aligned16(q_obs)) return fail(SNAP_ERR_INVALID_ARG, "q_obs is NULL or not 16-byte aligned");
   if (!k || !aligned16(k)) return fail(SNAP_ERR_INVALID_ARG, "k is NULL or not 16-byte aligned");
@@ -160,6 +166,11 @@ static snap_status check_prefill(const snap_params* p, int32_t n_seq, const int3
   if (n_seq < 0) return fail(SNAP_ERR_INVALID_ARG, "n_seq must be >= 0");
   if (n_seq == 0) return SNAP_OK;
   if (max_len < 1 || max_len > (1 << 28)) return fail(SNAP_ERR_INVALID_ARG, "max_len must be in [1, 2^28]");
+  const long long groups = (long long)n_seq * p->n_kv_heads;
+  const long long positions = G <= 4 ? 128 / G : 16;  // query positions per attention workgroup
+  if (groups > kMaxGridY || 8 * ((groups + 7) / 8) * ((max_len + positions - 1) / positions) > 0x7fffffffLL)
+    return fail(SNAP_ERR_UNSUPPORTED, "n_seq * n_kv_heads (%lld) and max_len (%d) exceed the launch grid", groups,
+                max_len);
   if (!lengths) return fail(SNAP_ERR_INVALID_ARG, "lengths is NULL");
   if (!q || !aligned16(q) || !k || !aligned16(k) || !v || !aligned16(v))
     return fail(SNAP_ERR_INVALID_ARG, "q, k and v must be non-NULL and 16-byte aligned");
@@ -228,6 +239,8 @@ snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, cons
   if ((st = check_cache(p, cache)) != SNAP_OK) return st;
   if (n < 0) return fail(SNAP_ERR_INVALID_ARG, "n must be >= 0");
   if (n == 0) return SNAP_OK;
+  if ((long long)n * p->n_q_heads > kMaxGridY)
+    return fail(SNAP_ERR_UNSUPPORTED, "n * n_q_heads must be at most %d", kMaxGridY);
   if (!pos || !n_topk || !slot_ids) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids NULL");
   if (!q || !aligned16(q)) return fail(SNAP_ERR_INVALID_ARG, "q is NULL or not 16-byte aligned");
   if (!out || !aligned16(out)) return fail(SNAP_ERR_INVALID_ARG, "out is NULL or not 16-byte aligned");
@@ -251,6 +264,8 @@ snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, cons
   if ((st = check_cache(p, cache)) != SNAP_OK) return st;
   if (n < 0) return fail(SNAP_ERR_INVALID_ARG, "n must be >= 0");
   if (n == 0) return SNAP_OK;
+  if ((long long)n * p->n_q_heads > kMaxGridY)
+    return fail(SNAP_ERR_UNSUPPORTED, "n * n_q_heads must be at most %d", kMaxGridY);
   if (!pos || !n_topk || !slot_ids) return fail(SNAP_ERR_INVALID_ARG, "pos/n_topk/slot_ids NULL");
   if (!q || !aligned16(q)) return fail(SNAP_ERR_INVALID_ARG, "q is NULL or not 16-byte aligned");
   if (!k_new || !aligned16(k_new)) return fail(SNAP_ERR_INVALID_ARG, "k_new is NULL or not 16-byte aligned");

@@ -123,7 +123,7 @@ __device__ __forceinline__ float lanes4_max(float x) {
 //                 reduction over the four lane groups;
 //   O^T += V^T P^T (A = V^T fragment from LDS, B = the probabilities exactly
 //                 as the first product left them in registers, cast to bf16).
-// K and V^T tiles each have two LDS stages, filled by direct loads.
+// Two LDS stages, each a K tile then a V^T tile, filled by direct loads.
 template <int KS>
 __global__ __launch_bounds__(256) void prefill_attn(PrefillArgs a) {
   constexpr int D = KS * 32;
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256) void prefill_attn(PrefillArgs a) {
   constexpr int kKBytes = kPfTK * D * 2;
   constexpr int kLoadsPerWave = CPR / kPfNW;  // per tile and per operand
   static_assert(CPR % kPfNW == 0, "equal loads per wave");
-  __shared__ __align__(16) unsigned char lds[4 * kKBytes];  // two K stages, two V^T stages
+  __shared__ __align__(16) unsigned char lds[4 * kKBytes];  // two stages of (K tile, V^T tile)
 
   const int lane = tid() & 63, wave = tid() >> 6;
   const int l16 = lane & 15, lg = lane >> 4;
@@ -217,8 +217,8 @@ __global__ __launch_bounds__(256) void prefill_attn(PrefillArgs a) {
   // one tile: keys [t0, t0+64) in stage st; the next tile loads into st_next
   auto step = [&](int i, const unsigned char* st, unsigned char* st_next) {
     const int t0 = i * kPfTK;
-    wait_vm<0>();
-    lds_barrier();
+    wait_vm<0>();   // this wave's part of tile i
+    lds_barrier();  // every wave's part; every wave is done with tile i-1 (stage st_next)
     if (i + 1 < nt) issue(t0 + kPfTK, st_next);
     f32x4 s[2][4];
 #pragma unroll

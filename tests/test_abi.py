@@ -222,3 +222,17 @@ def test_fp8_qk_validation():
     # a supported fp8 setting fails later (the fake cache has no scales), not on fp8_qk
     st, msg = _compress_status(_params(fp8_qk=1, kv_dtype=snap.SNAP_FP8_E4M3))
     assert st == snap.SNAP_ERR_INVALID_ARG and "scale" in msg
+
+
+def test_launch_grid_limits():
+    """Sizes whose per-(sequence, head) launch grids would not fit are refused
+    before any launch."""
+    L = snap.lib()
+    p = _params()
+    assert _compress_status(p, n_seq=8192)[0] == snap.SNAP_ERR_UNSUPPORTED  # 8192 x 8 KV heads
+    cache = snap.SnapCache(FAKE, FAKE, None, None, 4)
+    st = L.snap_decode_attn(ctypes.byref(p.c()), ctypes.byref(cache), FAKE, FAKE, 4096, FAKE, FAKE, FAKE,
+                            snap.SNAP_BF16, FAKE, 1 << 34, None)
+    assert st == snap.SNAP_ERR_UNSUPPORTED  # 4096 x 32 query heads
+    st = L.snap_prefill_attn(ctypes.byref(p.c()), 64, FAKE, 1 << 28, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 62, None)
+    assert st == snap.SNAP_ERR_UNSUPPORTED  # 512 groups x 2^23 position blocks
