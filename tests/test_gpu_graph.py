@@ -106,3 +106,51 @@ def test_graph_replay_fp32_two_launch_path():
     wl = synth.WORKLOADS["tiny-fp32"]
     print("\n[case] graph replay: fp32 decode step (append + attend launches), 4 replays", flush=True)
     _graph_vs_eager(wl, params_of(wl), [1024, 700], 4)
+
+
+def test_graph_replay_prefill():
+    """snap_prefill (V transpose, attention with the window statistics, then
+    the compression) captured once and replayed on new prompts of the same
+    lengths: every replay matches the eager call bit for bit (attention
+    output, cache bytes, selection, metadata)."""
+    wl = synth.Workload("graph-prefill", 15, 8, 2, 128, 128, False, 4, 32, 100, 32, 7, "bf16", "bf16", layers=1,
+                        batch=2, length=None, length_range=(64, 1000), decode_steps=0, rope=True, plant_frac=0.01)
+    p = params_of(wl)
+    lengths = [900, 333]
+    print(f"\n[case] graph replay: snap_prefill, lengths {lengths}, 3 replays", flush=True)
+    dev = "cuda"
+    n, ml = len(lengths), max(lengths)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.arange(n, dtype=torch.int32, device=dev)
+    q0, k0, v0 = (x.to(dev) for x in synth.prompt_batch(wl, 0, lengths))
+    sq, sk, sv = torch.empty_like(q0), torch.empty_like(k0), torch.empty_like(v0)
+    cg, ce = GpuCache(p, n), GpuCache(p, n)
+    ws_g = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    ws_e = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    out_g = torch.zeros((n, p.n_q_heads, ml, p.d_v), dtype=torch.bfloat16, device=dev)
+    out_e = torch.zeros_like(out_g)
+    sel_g = torch.zeros((n, p.n_kv_heads, p.topk), dtype=torch.int32, device=dev)
+    sel_e = torch.zeros_like(sel_g)
+    sq.copy_(q0)
+    sk.copy_(k0)
+    sv.copy_(v0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        snap.snap_prefill(p, cg.c(), cg.pos, cg.n_topk, sl, lens, sq, sk, sv, out_g, ws_g, sel_g)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        q, k, v = (x.to(dev) for x in synth.prompt_batch(wl, 0, lengths, salt=rep + 1))
+        sq.copy_(q)
+        sk.copy_(k)
+        sv.copy_(v)
+        torch.cuda.synchronize()
+        g.replay()
+        snap.snap_prefill(p, ce.c(), ce.pos, ce.n_topk, sl, lens, sq, sk, sv, out_e, ws_e, sel_e)
+        torch.cuda.synchronize()
+        assert torch.equal(out_g.view(torch.int16), out_e.view(torch.int16)), rep
+        assert torch.equal(sel_g, sel_e), rep
+        assert torch.equal(cg.k.view(torch.int16), ce.k.view(torch.int16)), rep
+        assert torch.equal(cg.v.view(torch.int16), ce.v.view(torch.int16)), rep
+        assert torch.equal(cg.pos, ce.pos) and torch.equal(cg.n_topk, ce.n_topk), rep
+        _ = torch.zeros(1 << 20, device="cuda").sum()  # eager work between replays
