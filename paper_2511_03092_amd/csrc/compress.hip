@@ -6,6 +6,8 @@
 // Kernel sequence per call (one stream, no host synchronisation):
 //   score_pass<STATS>   per (seq, KV head, key chunk): bf16 MFMA Q_obs x K^T,
 //                       per-row running max / sum-exp of the softmax domain
+//                       (skipped after the prefill attention, which writes
+//                       those statistics itself)
 //   stats_reduce        per (seq, KV head): row max + normaliser (fp64), and
 //                       the reset of the selection scratch
 //   score_pass<COLSUM>  recompute the scores, W = exp(z - c) * inv, column
