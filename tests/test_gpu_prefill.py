@@ -61,10 +61,10 @@ def _check_attention(p, lengths, q, k, v, out):
     return worst
 
 
-def _run(wl, p, lengths, slots=None, n_slots=None, band_rtol=BAND_RTOL):
+def _run(wl, p, lengths, slots=None, n_slots=None, band_rtol=BAND_RTOL, max_len=None):
     slots = list(range(len(lengths))) if slots is None else slots
     n_slots = len(lengths) if n_slots is None else n_slots
-    q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, slots, n_slots)
+    q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, slots, n_slots, max_len=max_len)
     err = _check_attention(p, lengths, q, k, v, out)
     qobs = oracle.window_queries(oracle_params(p), lengths, q)
     st = check_compress(p, cache, qobs, k, v, lengths, slots, sel, pooled)
@@ -96,9 +96,10 @@ def test_prefill_group_sizes(hq, hkv, d):
 def test_prefill_short_prompts_and_window_longer_than_prompt():
     wl = synth.small(GQA, sink=8, recent=16, topk=20, obs_window=32)
     p = params_of(wl)
-    lengths = [20, 24, 25, 31, 45, 2]
-    _announce(f"snap_prefill short prompts (L <= sink+recent, L < w): lengths {lengths}")
-    _run(wl, p, lengths)
+    lengths = [20, 24, 25, 31, 45, 2, 0]
+    _announce(f"snap_prefill short prompts (L <= sink+recent, L < w, an empty prompt), padded to 300: "
+              f"lengths {lengths}")
+    _run(wl, p, lengths, max_len=300)
 
 
 def test_prefill_streaming_only():
