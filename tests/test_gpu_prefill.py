@@ -251,3 +251,54 @@ def test_prefill_into_fp8_cache(scales):
     st = check_compress(p, cache, qobs, k, v, lengths, slots, gsel, pooled.cpu().numpy())
     print(f"  swaps {st['swaps']}, decision band {st['band_rel_err']:.3e}", flush=True)
     assert st["band_rel_err"] <= BAND_RTOL
+
+
+def test_prefill_full_size_llama_batch_128k():
+    """One layer of the 8-prompt Llama batch (72k-131k tokens) at full size, as
+    `bench.py --prefill --workload llama8b-32layer-b8-128k` runs it: sampled
+    output rows of sampled heads of the longest and shortest prompts against
+    the oracle one by one, and the selection of two (prompt, KV head) units
+    against the oracle's compression."""
+    wl = synth.WORKLOADS["llama8b-32layer-b8-128k"]
+    p = params_of(wl)
+    lengths = synth.draw_lengths(wl, 0, wl.batch)
+    n, ml = len(lengths), max(lengths)
+    _announce(f"snap_prefill llama8b-32layer-b8-128k layer 0 at full size: lengths {lengths}")
+    dev = "cuda"
+    q, k, v = synth.prompt_batch(wl, 0, lengths, device=dev, max_len=ml, pad_value=float("nan"))
+    cache = GpuCache(p, n)
+    ws = snap.workspace(snap.snap_prefill_workspace(p, n, ml))
+    out = torch.empty((n, p.n_q_heads, ml, p.d_v), dtype=torch.bfloat16, device=dev)
+    sel = torch.empty((n, p.n_kv_heads, p.topk), dtype=torch.int32, device=dev)
+    pooled = torch.empty((n, p.n_kv_heads, ml), dtype=torch.float32, device=dev)
+    lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
+    sl = torch.arange(n, dtype=torch.int32, device=dev)
+    snap.snap_prefill(p, cache.c(), cache.pos, cache.n_topk, sl, lens, q, k, v, out, ws, sel, pooled)
+    torch.cuda.synchronize()
+    op = oracle_params(p)
+    G = op.group
+    gen = np.random.default_rng(11)
+    worst, worst_band = 0.0, 0.0
+    for b in [int(np.argmax(lengths)), int(np.argmin(lengths))]:
+        L = lengths[b]
+        assert torch.isfinite(out[b, :, :L].float()).all()
+        qc, kc, vc = oracle.f64(q[b]), oracle.f64(k[b]), oracle.f64(v[b])
+        rows = sorted(set([0, 63, 64, L - 33, L - 1] + gen.integers(0, L, 3).tolist()))
+        worst = max(worst, _sampled_rows(p, qc, kc, vc, out[b], L, rows, [0, 17, 31]))
+        qobs = oracle.window_queries(op, [L], qc[None])
+        g = int(gen.integers(0, p.n_kv_heads))
+        res = oracle.compress_group(op, L, qobs[0, g * G:(g + 1) * G], kc[g, :L], vc[g, :L])
+        gs = sel[b, g].cpu().numpy()
+        swaps = check_selection(gs, res.P, L, p.sink, p.recent, p.topk)
+        P = res.P[p.sink:L - p.recent]
+        gp = pooled[b, g, p.sink:L - p.recent].double().cpu().numpy()
+        keff = min(L - p.sink - p.recent, p.topk)
+        tau = np.sort(P)[::-1][keff - 1]
+        band = (P >= tau / 4) & (P <= 4 * tau)
+        rel = float((np.abs(gp - P) / np.maximum(P, 1e-30))[band].max())
+        worst_band = max(worst_band, rel)
+        ek = oracle.assemble(L, p.sink, p.recent, p.topk, kc[g, :L], gs[:keff])
+        assert np.array_equal(cache.k[b, g].double().cpu().numpy(), ek)
+        print(f"  prompt {b} (L={L}), head {g}: swaps {swaps}, band rel err {rel:.3e}", flush=True)
+    print(f"  sampled attention max abs err {worst:.3e}", flush=True)
+    assert worst_band <= BAND_RTOL
