@@ -302,3 +302,13 @@ def test_prefill_full_size_llama_batch_128k():
         print(f"  prompt {b} (L={L}), head {g}: swaps {swaps}, band rel err {rel:.3e}", flush=True)
     print(f"  sampled attention max abs err {worst:.3e}", flush=True)
     assert worst_band <= BAND_RTOL
+
+
+def test_prefill_avg_pool_kernel13_explicit_scale():
+    """Average pooling with the Table 6 kernel (13) and an explicit softmax
+    scale, which the attention and the window statistics both take."""
+    wl = synth.small(GQA, pool=synth.POOL_AVG, pool_kernel=13)
+    p = params_of(wl, sm_scale=0.05)
+    lengths = [950, 500]
+    _announce(f"snap_prefill avg pool, kernel 13, sm_scale 0.05: lengths {lengths}")
+    _run(wl, p, lengths)
