@@ -167,7 +167,7 @@ static snap_status check_prefill(const snap_params* p, int32_t n_seq, const int3
   if (n_seq == 0) return SNAP_OK;
   if (max_len < 1 || max_len > (1 << 28)) return fail(SNAP_ERR_INVALID_ARG, "max_len must be in [1, 2^28]");
   const long long groups = (long long)n_seq * p->n_kv_heads;
-  const long long positions = G <= 4 ? 128 / G : 16;  // query positions per attention workgroup
+  const long long positions = 256 / G;  // query positions per attention workgroup
   if (groups > kMaxGridY || 8 * ((groups + 7) / 8) * ((max_len + positions - 1) / positions) > 0x7fffffffLL)
     return fail(SNAP_ERR_UNSUPPORTED, "n_seq * n_kv_heads (%lld) and max_len (%d) exceed the launch grid", groups,
                 max_len);

@@ -27,7 +27,7 @@
 namespace snap {
 
 constexpr int kPfTK = 64;  // keys per tile
-constexpr int kPfNW = 4;   // waves per workgroup, 32 query rows each
+constexpr int kPfNW = 8;   // waves per workgroup, 32 query rows each
 
 struct PrefillArgs {
   const uint16_t* q;   // [n_seq][Hq][max_len][D]
@@ -43,22 +43,18 @@ struct PrefillArgs {
   float scale2;        // softmax scale * log2(e), rounded to fp32
 };
 
-// Query positions per workgroup for G heads per KV head: the 128 rows of a
+// Query positions per workgroup for G heads per KV head: the 256 rows of a
 // workgroup are (head, position) pairs of one KV head, so every key tile in
 // LDS serves all G heads.
-static inline int prefill_positions(int G) { return G <= 4 ? 128 / G : 16; }
+static inline int prefill_positions(int G) { return 256 / G; }
 
 // Head within the group and position offset within the workgroup of row block
-// rb (16 rows) of wave w.  G <= 4: each wave owns one head and 32 consecutive
-// positions; G == 8: each wave owns two heads at the same 16 positions.
+// rb (16 rows) of wave w: the workgroup's 16 row blocks run over the G heads
+// fastest, then over blocks of 16 positions.
 __device__ __forceinline__ void pf_rowblock(int G, int w, int rb, int& hl, int& po) {
-  if (G <= 4) {
-    hl = w % G;
-    po = 32 * (w / G) + 16 * rb;
-  } else {
-    hl = 2 * w + rb;
-    po = 0;
-  }
+  const int rbi = 2 * w + rb;
+  hl = rbi % G;
+  po = 16 * (rbi / G);
 }
 
 // Key order of V^T within each 32-key group: stored position u = 8q + 4h + e
@@ -116,7 +112,7 @@ __device__ __forceinline__ float lanes4_max(float x) {
 
 // One workgroup per (KV head group bg, block kb of P query positions counted
 // from the end of the prompt: block 0 holds positions [L-P, L), the window).
-// Rows: 4 waves x 32 (head, position) pairs.  Products, per 64-key tile:
+// Rows: 8 waves x 32 (head, position) pairs.  Products, per 64-key tile:
 //   S^T = K Q^T   (A = K fragment from LDS, B = Q fragment held in registers):
 //                 lane l gets query row l%16 against keys 4*(l/16)+e of each
 //                 16-key block, so a row's softmax is lane-local up to a
@@ -125,7 +121,7 @@ __device__ __forceinline__ float lanes4_max(float x) {
 //                 as the first product left them in registers, cast to bf16).
 // Two LDS stages, each a K tile then a V^T tile, filled by direct loads.
 template <int KS>
-__global__ __launch_bounds__(256) void prefill_attn(PrefillArgs a) {
+__global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
   constexpr int D = KS * 32;
   constexpr int CPR = D / 8;   // 16-byte chunks per key row
   constexpr int DVB = D / 16;  // value blocks of 16 dims
@@ -439,9 +435,9 @@ snap_status launch_prefill_attn(const snap_params& p, int n_seq, const int32_t* 
   pa.groups = groups;
   dim3 grid(8 * ((groups + 7) / 8) * pa.n_qblocks);
   if (p.d_qk == 128)
-    hipLaunchKernelGGL(prefill_attn<4>, grid, dim3(256), 0, stream, pa);
+    hipLaunchKernelGGL(prefill_attn<4>, grid, dim3(512), 0, stream, pa);
   else
-    hipLaunchKernelGGL(prefill_attn<2>, grid, dim3(256), 0, stream, pa);
+    hipLaunchKernelGGL(prefill_attn<2>, grid, dim3(512), 0, stream, pa);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
   return SNAP_OK;
 }
