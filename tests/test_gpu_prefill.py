@@ -93,6 +93,20 @@ def test_prefill_group_sizes(hq, hkv, d):
     _run(wl, p, lengths)
 
 
+@pytest.mark.parametrize("hq,hkv,d,w,recent,norm", [(8, 1, 64, 32, 16, synth.NORM_CAND),
+                                                    (8, 2, 128, 64, 40, synth.NORM_ROW)])
+def test_prefill_largest_window(hq, hkv, d, w, recent, norm):
+    """The largest window (G * w = 256 score rows: exactly one attention
+    workgroup's block of 256 / G positions) with w > recent, so the causal
+    mask also cuts the candidate domain of the first window rows."""
+    wl = synth.small(GQA, n_q_heads=hq, n_kv_heads=hkv, d_qk=d, d_v=d, obs_window=w, recent=recent, norm=norm)
+    p = params_of(wl)
+    lengths = [700, 161, 90, 50]
+    _announce(f"snap_prefill window {w} = one block of {256 // (hq // hkv)} positions, G={hq // hkv} D={d} "
+              f"recent={recent} norm={'cand' if norm == 0 else 'row'}: lengths {lengths}")
+    _run(wl, p, lengths)
+
+
 def test_prefill_short_prompts_and_window_longer_than_prompt():
     wl = synth.small(GQA, sink=8, recent=16, topk=20, obs_window=32)
     p = params_of(wl)
