@@ -713,6 +713,18 @@ def run_prefill(args, wl):
     print(json.dumps(res), flush=True)
 
 
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None where it is not readable."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
     """The fp64 oracle's causal attention on the host's cores, on a bounded
     sample: the last rows of one query head at the longest prompt (each row
@@ -762,7 +774,7 @@ def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
     val1 = tokens / (total_macs / rate1)
     valT = tokens / (total_macs / rateT)
     return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
-            "single_thread_value": float(f"{val1:.6g}"),
+            "cpu_model": cpu_model(), "single_thread_value": float(f"{val1:.6g}"),
             "sample": (f"causal attention rows {L - nrow}..{L - 1} of one head at L={L} (fp64 oracle): "
                        f"{t1:.2f} s on one thread, the same rows of {T} heads on {T} threads in {tT:.2f} s; "
                        f"extrapolated by multiply-adds to every head and position of {len(lengths)} prompt(s), "
@@ -830,7 +842,7 @@ def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_valu
     val1 = tokens / (t_comp1 * scale + t_dec1 * units_dec)
     valT = tokens / (t_compT * scale + t_decT * units_dec)
     return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
-            "single_thread_value": float(f"{val1:.6g}"),
+            "cpu_model": cpu_model(), "single_thread_value": float(f"{val1:.6g}"),
             "sample": (f"compress units (1 sequence x 1 KV head, L={L}): 1 alone at {t_comp1:.2f} s, then {T} "
                        f"on {T} threads at {t_compT:.2f} s each; decode units (1 sequence x 1 KV head x 1 "
                        f"step): {n_dec} alone at {t_dec1 * 1e3:.1f} ms, then {T * per} on {T} threads at "
