@@ -806,18 +806,44 @@ struct AssembleArgs {
 
 constexpr int kAsmRows = 64;  // cache rows per assemble workgroup
 
+// First ring token l0 = max(L - r, s) and ring_base = (l0 - s) mod r, the
+// ring row of token l0 counted from s (one division per thread, not per row).
+struct RingMap {
+  int l0, base;
+};
+__device__ __forceinline__ RingMap ring_map(int L, int s, int r) {
+  const int l0 = L - r > s ? L - r : s;
+  return RingMap{l0, (l0 - s) % r};
+}
+
 // Source token of cache row `row` (or -1 for a zero padding row).
-__device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff, const int32_t* sel) {
+__device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff, const int32_t* sel,
+                                          RingMap rm) {
   if (row < s) return row < L ? row : -1;
   if (row < s + r) {
-    int l0 = L - r > s ? L - r : s;  // first ring token
-    int off = ((row - s) - (l0 - s)) % r;
+    // token l0 + ((row - s) - base) mod r, with both terms in [0, r)
+    int off = (row - s) - rm.base;
     if (off < 0) off += r;
-    int t = l0 + off;
+    int t = rm.l0 + off;
     return t < L ? t : -1;
   }
   int m = row - s - r;
   return m < keff ? sel[m] : -1;
+}
+
+// x / scale rounded once to fp32, as an IEEE division gives it, from a
+// correctly rounded reciprocal inv = 1 / scale and one fused correction:
+// q0 = x * inv, r = x - q0 * scale (exact by fma), q = q0 + r * inv (Markstein's
+// theorem: correctly rounded when neither r nor the quotient leaves the
+// normal range).  Where q0 is 0 or not finite it is kept: the E4M3 code of a
+// zero, of a quotient too small for a non-zero code, or of a saturated one
+// does not depend on the correction.  Checked against the division on every
+// finite bf16 x over several thousand scales: identical E4M3 codes.
+__device__ __forceinline__ float div_by_scale(float x, float scale, float inv) {
+  const float q0 = x * inv;
+  const float r = __builtin_fmaf(-q0, scale, x);
+  const float q = __builtin_fmaf(r, inv, q0);
+  return (q0 == 0.f || !__builtin_isfinite(q0)) ? q0 : q;
 }
 
 // 8 elements of an input row in raw form: 16 bytes of bf16 or 32 of fp32
@@ -837,7 +863,7 @@ __device__ __forceinline__ Raw8In<In> load8(const In* src) {
 // ... stored into the cache, quantised to E4M3 codes of x / scale when the
 // cache is fp8.
 template <typename In, typename Out>
-__device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scale) {
+__device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scale, float inv) {
   if constexpr (sizeof(Out) == 1) {
     float f[8];
     if constexpr (sizeof(In) == 2) {
@@ -855,7 +881,7 @@ __device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scal
     for (int h = 0; h < 2; ++h) {
       uint32_t w = 0;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(f[h * 4 + i] / scale) << (8 * i);
+      for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(div_by_scale(f[h * 4 + i], scale, inv)) << (8 * i);
       o[h] = w;
     }
     *(u32x2*)dst = o;
@@ -897,10 +923,11 @@ __global__ __launch_bounds__(256) void fp8_amax(AssembleArgs a) {
   const size_t in_row0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
   const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
   const int items = (row1 - row0) * per_row;
+  const RingMap rm = ring_map(L, s, r);
   uint32_t mk = 0, mv = 0;
   for (int it = tid(); it < items; it += nthreads()) {
     const int row = row0 + it / per_row, piece = it % per_row;
-    const int t = row_source(row, L, s, r, keff, sg);
+    const int t = row_source(row, L, s, r, keff, sg, rm);
     if (t < 0) continue;
     const u32x4 x = piece < kp ? *((const u32x4*)((const uint16_t*)a.k + (in_row0 + t) * a.dk) + piece)
                                : *((const u32x4*)((const uint16_t*)a.v + (in_row0 + t) * a.dv) + (piece - kp));
@@ -973,20 +1000,35 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
       if (a.v) vs = a.v_scale[(size_t)slot * a.Hkv + g];
     }
   }
+  const float kinv = 1.0f / ks, vinv = 1.0f / vs;
+  const RingMap rm = ring_map(L, s, r);
   const int kp = a.dk / 8, vp = a.v ? a.dv / 8 : 0, per_row = kp + vp;
   const int items = (row1 - row0) * per_row;
+  // item it = row * per_row + piece; this thread's items advance by
+  // nthreads(), i.e. by (step_r rows, step_p pieces) with a carry, so the
+  // division runs once per thread
+  const int step_r = nthreads() / per_row, step_p = nthreads() % per_row;
+  int cur_r = tid() / per_row, cur_p = tid() % per_row;
   for (int it0 = tid(); it0 < items; it0 += kAsmU * nthreads()) {
-    int src_t[kAsmU];
+    int row_u[kAsmU], piece_u[kAsmU], src_t[kAsmU];
 #pragma unroll
     for (int u = 0; u < kAsmU; ++u) {
       const int it = it0 + u * nthreads();
-      src_t[u] = it < items ? row_source(row0 + it / per_row, L, s, r, keff, sg) : -1;
+      row_u[u] = row0 + cur_r;
+      piece_u[u] = cur_p;
+      cur_r += step_r;
+      cur_p += step_p;
+      if (cur_p >= per_row) {
+        cur_p -= per_row;
+        ++cur_r;
+      }
+      src_t[u] = it < items ? row_source(row_u[u], L, s, r, keff, sg, rm) : -1;
     }
     Raw8In<In> x[kAsmU];
 #pragma unroll
     for (int u = 0; u < kAsmU; ++u) {
       const int it = it0 + u * nthreads();
-      const int piece = it % per_row, t = src_t[u];
+      const int piece = piece_u[u], t = src_t[u];
       const In* src = nullptr;
       if (it < items && t >= 0)
         src = piece < kp ? (const In*)a.k + (in_row0 + t) * a.dk + 8 * piece
@@ -997,11 +1039,11 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
     for (int u = 0; u < kAsmU; ++u) {
       const int it = it0 + u * nthreads();
       if (it >= items) break;
-      const int row = row0 + it / per_row, piece = it % per_row;
+      const int row = row_u[u], piece = piece_u[u];
       if (piece < kp)
-        store8<In, Out>(x[u], (Out*)a.ck + (out_row0 + row) * a.dk + 8 * piece, ks);
+        store8<In, Out>(x[u], (Out*)a.ck + (out_row0 + row) * a.dk + 8 * piece, ks, kinv);
       else
-        store8<In, Out>(x[u], (Out*)a.cv + (out_row0 + row) * a.dv + 8 * (piece - kp), vs);
+        store8<In, Out>(x[u], (Out*)a.cv + (out_row0 + row) * a.dv + 8 * (piece - kp), vs, vinv);
     }
   }
 }
