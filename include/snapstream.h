@@ -196,7 +196,7 @@ size_t snap_prefill_workspace(const snap_params* p, int32_t n_seq, int32_t max_l
  *   workspace >= snap_prefill_workspace(p, n_seq, max_len) bytes, 256-byte
  *             aligned; its contents on entry do not matter.
  * Supported: in_dtype bf16, d_qk == d_v in {64, 128} (v_in_k = 0), and
- * G = n_q_heads / n_kv_heads in {1, 2, 4, 8}; SNAP_ERR_UNSUPPORTED otherwise.
+ * G = n_q_heads / n_kv_heads in {1, 2, 4, 8, 16}; SNAP_ERR_UNSUPPORTED otherwise.
  * out must not alias q, k or v.  n_seq == 0 is a no-op. */
 snap_status snap_prefill(const snap_params* p, const snap_cache* cache, int32_t* pos, int32_t* n_topk,
                          int32_t n_seq, const int32_t* slot_ids, const int32_t* lengths, int32_t max_len,

@@ -161,8 +161,8 @@ static snap_status check_prefill(const snap_params* p, int32_t n_seq, const int3
   if (p->v_in_k || p->d_qk != p->d_v || (p->d_qk != 64 && p->d_qk != 128))
     return fail(SNAP_ERR_UNSUPPORTED, "snap_prefill supports d_qk == d_v in {64, 128} with a separate V");
   const int G = p->n_q_heads / p->n_kv_heads;
-  if (G != 1 && G != 2 && G != 4 && G != 8)
-    return fail(SNAP_ERR_UNSUPPORTED, "snap_prefill supports 1, 2, 4 or 8 query heads per KV head (got %d)", G);
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+    return fail(SNAP_ERR_UNSUPPORTED, "snap_prefill supports 1, 2, 4, 8 or 16 query heads per KV head (got %d)", G);
   if (n_seq < 0) return fail(SNAP_ERR_INVALID_ARG, "n_seq must be >= 0");
   if (n_seq == 0) return SNAP_OK;
   if (max_len < 1 || max_len > (1 << 28)) return fail(SNAP_ERR_INVALID_ARG, "max_len must be in [1, 2^28]");

@@ -188,7 +188,7 @@ def test_prefill_validation():
     # unsupported shapes and dtypes
     assert pre(params=_params(in_dtype=snap.SNAP_F32, kv_dtype=snap.SNAP_F32)) == snap.SNAP_ERR_UNSUPPORTED
     assert pre(params=_params(n_q_heads=48, n_kv_heads=4)) == snap.SNAP_ERR_UNSUPPORTED  # G = 12
-    assert pre(params=_params(n_q_heads=16, n_kv_heads=1, obs_window=16)) == snap.SNAP_ERR_UNSUPPORTED  # G = 16
+    assert pre(params=_params(n_q_heads=24, n_kv_heads=4, obs_window=16)) == snap.SNAP_ERR_UNSUPPORTED  # G = 6
     lat = _params(n_q_heads=8, n_kv_heads=1, d_qk=576, d_v=512, v_in_k=1, recent=4096, topk=28668)
     lcache = snap.SnapCache(FAKE, None, None, None, 4)
     assert L.snap_prefill(ctypes.byref(lat.c()), ctypes.byref(lcache), FAKE, FAKE, 1, FAKE, FAKE, 4096, FAKE, FAKE,

@@ -84,7 +84,7 @@ def test_prefill_gqa_ragged_batch(norm):
     _run(wl, p, lengths, slots=[2, 0, 3, 1], n_slots=5)
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 64), (8, 4, 64), (8, 1, 64), (16, 2, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 64), (8, 4, 64), (8, 1, 64), (16, 2, 128), (16, 1, 128), (32, 2, 64)])
 def test_prefill_group_sizes(hq, hkv, d):
     wl = synth.small(GQA, n_q_heads=hq, n_kv_heads=hkv, d_qk=d, d_v=d, obs_window=16)
     p = params_of(wl)
