@@ -962,8 +962,12 @@ struct CombineArgs {
 
 constexpr int kMaxChunks = 512;
 constexpr int kCombineThreads = 128;
+constexpr int kCombineRegChunks = 32;  // partials loaded ahead into registers
 // grid (n * Hq, ceil(dv / 128)): the chunk weights exp2(m_c - M) are formed
 // once per workgroup in LDS, then each thread sums its value dim over chunks.
+// The thread's first 32 partials are loaded before the weights are formed, so
+// their latency overlaps the (m, l) loads and reductions instead of following
+// them.
 __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   __shared__ float wts[kMaxChunks];
   __shared__ float red[kCombineThreads / 64];
@@ -971,6 +975,12 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   const int slot = a.slot_ids[b];
   if (slot < 0 || slot >= a.n_slots) return;
   const int lane = tid() & 63, wave = tid() >> 6;
+  const int d = bid_y() * kCombineThreads + tid();
+  const float* part = a.part + (size_t)bh * a.n_chunks * a.dv + d;
+  const int nreg = d < a.dv ? min(a.n_chunks, kCombineRegChunks) : 0;
+  float pr[kCombineRegChunks];
+#pragma unroll
+  for (int c = 0; c < kCombineRegChunks; ++c) pr[c] = c < nreg ? part[(size_t)c * a.dv] : 0.f;
   const float2* ml = a.ml + (size_t)bh * a.n_chunks;
   float M = -INFINITY;
   for (int c = tid(); c < a.n_chunks; c += nthreads()) M = fmaxf(M, ml[c].x);
@@ -994,11 +1004,25 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   float wsum = 0.f;
   for (int i = 0; i < kCombineThreads / 64; ++i) wsum += red[i];
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  const int d = bid_y() * kCombineThreads + tid();
   if (d >= a.dv) return;
-  const float* part = a.part + (size_t)bh * a.n_chunks * a.dv + d;
+  // four accumulators over chunks c = 0, 4, 8, ... / 1, 5, ... (groups of
+  // four while they are whole), the remaining chunks into the first
   float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
-  int c = 0;
+  const int nfull = a.n_chunks & ~3;
+#pragma unroll
+  for (int cc = 0; cc < kCombineRegChunks; cc += 4) {
+    if (cc + 4 <= nfull) {
+      o0 = fmaf(wts[cc], pr[cc], o0);
+      o1 = fmaf(wts[cc + 1], pr[cc + 1], o1);
+      o2 = fmaf(wts[cc + 2], pr[cc + 2], o2);
+      o3 = fmaf(wts[cc + 3], pr[cc + 3], o3);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (cc + e < nreg) o0 = fmaf(wts[cc + e], pr[cc + e], o0);
+    }
+  }
+  int c = kCombineRegChunks;
   for (; c + 4 <= a.n_chunks; c += 4) {
     o0 = fmaf(wts[c], part[(size_t)c * a.dv], o0);
     o1 = fmaf(wts[c + 1], part[(size_t)(c + 1) * a.dv], o1);
