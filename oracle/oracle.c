@@ -119,13 +119,18 @@ void oracle_pool(int64_t L, int s, int r, int kp, int pool, const double* A,
   }
 }
 
-static const double* g_sort_key;
+/* A candidate and its pooled score, so the ranking comparator needs no state
+ * outside its arguments (the oracle runs units on several threads at once). */
+typedef struct {
+  double p;
+  int64_t t;
+} ranked;
 static int cmp_rank(const void* a, const void* b) {
-  int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
-  double px = g_sort_key[x], py = g_sort_key[y];
-  if (px > py) return -1; /* larger pooled score first */
-  if (px < py) return 1;
-  return (x < y) ? -1 : (x > y); /* equal scores: lower token index first */
+  const ranked* x = (const ranked*)a;
+  const ranked* y = (const ranked*)b;
+  if (x->p > y->p) return -1; /* larger pooled score first */
+  if (x->p < y->p) return 1;
+  return (x->t < y->t) ? -1 : (x->t > y->t); /* equal scores: lower token index first */
 }
 static int cmp_i64(const void* a, const void* b) {
   int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
@@ -141,14 +146,19 @@ int oracle_topk(int64_t L, int s, int r, int K, const double* P, int32_t* sel) {
   int64_t c0 = s, c1 = L - r;
   int64_t n = c1 - c0;
   if (n <= 0 || K <= 0) return 0;
-  int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
-  for (int64_t t = 0; t < n; ++t) idx[t] = c0 + t;
-  g_sort_key = P;
-  qsort(idx, (size_t)n, sizeof(int64_t), cmp_rank);
+  ranked* rk = (ranked*)malloc(sizeof(ranked) * (size_t)n);
+  for (int64_t t = 0; t < n; ++t) {
+    rk[t].p = P[c0 + t];
+    rk[t].t = c0 + t;
+  }
+  qsort(rk, (size_t)n, sizeof(ranked), cmp_rank);
   int keff = (int)(n < K ? n : K);
+  int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)keff);
+  for (int m = 0; m < keff; ++m) idx[m] = rk[m].t;
   qsort(idx, (size_t)keff, sizeof(int64_t), cmp_i64);
   for (int m = 0; m < keff; ++m) sel[m] = (int32_t)idx[m];
   free(idx);
+  free(rk);
   return keff;
 }
 

@@ -43,10 +43,11 @@ MUTANTS = [
      "P[j] = (pool == POOL_MAX) ? acc : acc / (double)(kp - 1 + (kp == 1));"),
     ("pool window leaks outside the candidates", "if (t < c0 || t >= c1) continue;",
      "if (t < 0 || t >= L) continue;"),
-    ("ties go to the higher index", "return (x < y) ? -1 : (x > y); /* equal scores",
-     "return (x > y) ? -1 : (x < y); /* equal scores"),
-    ("smallest pooled scores kept", "if (px > py) return -1; /* larger pooled score first */\n  if (px < py) return 1;",
-     "if (px < py) return -1; /* larger pooled score first */\n  if (px > py) return 1;"),
+    ("ties go to the higher index", "return (x->t < y->t) ? -1 : (x->t > y->t); /* equal scores",
+     "return (x->t > y->t) ? -1 : (x->t < y->t); /* equal scores"),
+    ("smallest pooled scores kept",
+     "if (x->p > y->p) return -1; /* larger pooled score first */\n  if (x->p < y->p) return 1;",
+     "if (x->p < y->p) return -1; /* larger pooled score first */\n  if (x->p > y->p) return 1;"),
     ("ring rows stored linearly", "int row = oracle_slot_of(t, s, r);", "int row = (int)(t - lo + s);"),
     ("kept rows read one token early", "x + (size_t)sel[m] * width", "x + (size_t)(sel[m] - (sel[m] > 0)) * width"),
     ("decode misses the new token", "int n1 = (int)((p + 1) < (int64_t)(s + r) ? (p + 1) : (int64_t)(s + r));",

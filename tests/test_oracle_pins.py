@@ -129,6 +129,21 @@ def test_topk_matches_stable_argsort():
     assert got.tolist() == sorted(order.tolist())
 
 
+def test_topk_on_many_threads_matches_one_thread():
+    """The oracle runs (sequence, KV head) units on threads at once: the
+    selection of every unit must equal the same unit's selection run alone
+    (no state shared between concurrent rankings)."""
+    from concurrent.futures import ThreadPoolExecutor
+    L, s, r, K = 20000, 4, 64, 3000
+    Ps = [np.round(np.random.default_rng(100 + i).random(L) * 1000) / 1000 for i in range(16)]
+    alone = [oracle.topk(L, s, r, K, P) for P in Ps]
+    for _ in range(3):
+        with ThreadPoolExecutor(8) as ex:
+            together = list(ex.map(lambda P: oracle.topk(L, s, r, K, P), Ps))
+        for a, b in zip(alone, together):
+            assert np.array_equal(a, b)
+
+
 # ---------------------------------------------------------------- Eq. 1 & 3
 def test_two_candidate_logistic_closed_form():
     """With exactly two candidates, Eq. 3's softmax is the logistic function of
