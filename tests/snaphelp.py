@@ -36,6 +36,28 @@ def oracle_params(p: snap.Params) -> oracle.Params:
                          p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
 
 
+# Canary bit patterns (a quiet NaN in each storage type, the E4M3 NaN code for
+# fp8): the cache starts filled with them, so a row the library fails to
+# write, or a row decode reads although it is not valid, shows up as a NaN.
+_RAW = {torch.float32: (torch.int32, 0x7FC00000), torch.bfloat16: (torch.int16, 0x7FC0),
+        torch.uint8: (torch.uint8, 0x7F)}
+
+
+def raw(t: torch.Tensor) -> torch.Tensor:
+    """The tensor's storage as integers (bit-exact comparisons, NaN-safe)."""
+    return t.view(_RAW[t.dtype][0])
+
+
+def fill_canary(t: torch.Tensor):
+    it, pat = _RAW[t.dtype]
+    t.view(it).fill_(pat)
+
+
+def is_canary(t: torch.Tensor) -> bool:
+    it, pat = _RAW[t.dtype]
+    return bool(torch.all(t.view(it) == pat))
+
+
 class GpuCache:
     """One layer's cache on the device plus slot metadata."""
 
@@ -44,8 +66,12 @@ class GpuCache:
         B = p.budget
         dt = {snap.SNAP_F32: torch.float32, snap.SNAP_BF16: torch.bfloat16, snap.SNAP_FP8_E4M3: torch.uint8}[p.kv_dtype]
         # canary-filled: rows the library must write are checked, others must stay untouched
-        self.k = torch.full((n_slots, p.n_kv_heads, B, p.d_qk), 0, dtype=dt, device=dev)
-        self.v = None if p.v_in_k else torch.full((n_slots, p.n_kv_heads, B, p.d_v), 0, dtype=dt, device=dev)
+        self.k = torch.empty((n_slots, p.n_kv_heads, B, p.d_qk), dtype=dt, device=dev)
+        fill_canary(self.k)
+        self.v = None
+        if not p.v_in_k:
+            self.v = torch.empty((n_slots, p.n_kv_heads, B, p.d_v), dtype=dt, device=dev)
+            fill_canary(self.v)
         self.k_scale = self.v_scale = None
         if p.kv_dtype == snap.SNAP_FP8_E4M3:
             self.k_scale = torch.ones((n_slots, p.n_kv_heads), dtype=torch.float32, device=dev)
@@ -68,6 +94,37 @@ class GpuCache:
                 return (x * sc.cpu().double()[:, :, None, None]).numpy()
             return t.cpu().double().numpy()
         return val(self.k, self.k_scale), val(self.v, self.v_scale)
+
+    def assert_untouched(self, slots):
+        """The given slots still hold the canary in every row, and their metadata."""
+        for s_ in slots:
+            assert is_canary(self.k[s_]), f"slot {s_}: K rows written"
+            if self.v is not None:
+                assert is_canary(self.v[s_]), f"slot {s_}: V rows written"
+            assert int(self.pos[s_]) == -1, f"slot {s_}: pos written"
+
+    def poison_invalid_rows(self, slots):
+        """Refill with the canary every row of these slots that decode must not
+        read at the next step: top-K padding rows past n_topk, and sink / ring
+        rows at or past the next token's position that no token filled yet
+        (the appends fill them before any step reads them)."""
+        s, r, K = self.p.sink, self.p.recent, self.p.topk
+        pos = self.pos.cpu().tolist()
+        nt = self.n_topk.cpu().tolist()
+        for s_ in slots:
+            p_, n_ = pos[s_], nt[s_]
+            rows = list(range(s + r + n_, s + r + K))
+            if p_ < s + r:
+                rows += list(range(max(p_, 0), s + r))
+            if not rows:
+                continue
+            idx = torch.tensor(rows, dtype=torch.long, device=self.k.device)
+            for t in (self.k, self.v):
+                if t is not None:
+                    view = t[s_]
+                    fill = torch.empty_like(view[:, idx])
+                    fill_canary(fill)
+                    view[:, idx] = fill
 
 
 def gpu_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, debug=True):
@@ -179,13 +236,71 @@ def fp8_query(q) -> np.ndarray:
     return out
 
 
+class OracleCache:
+    """The oracle's own cache (its own selection, its own fp8 scales) followed
+    step by step with the same appended tokens, for the end-to-end decode
+    error: GPU output against the oracle's decode over the oracle's cache."""
+
+    def __init__(self, p: snap.Params, res, lengths, scales=None):
+        """res: oracle.compress result; scales: per sequence (k_scale[Hkv],
+        v_scale[Hkv] or None) for fp8 caches with caller-given scales, None to
+        take the oracle's data scales of its own kept rows (or no fp8)."""
+        self.p = p
+        self.fp8 = p.kv_dtype == snap.SNAP_FP8_E4M3
+        n = len(lengths)
+        self.k = res.cache_k.copy()
+        self.v = None if res.cache_v is None else res.cache_v.copy()
+        self.ks = np.ones((n, p.n_kv_heads))
+        self.vs = np.ones((n, p.n_kv_heads))
+        if self.fp8:
+            for b in range(n):
+                for g in range(p.n_kv_heads):
+                    if scales is not None:
+                        self.ks[b, g] = scales[b][0][g]
+                        if self.v is not None:
+                            self.vs[b, g] = scales[b][1][g]
+                    else:
+                        self.ks[b, g] = oracle.fp8_scale(self.k[b, g])
+                        if self.v is not None:
+                            self.vs[b, g] = oracle.fp8_scale(self.v[b, g])
+                    self.k[b, g] = self._q(self.k[b, g], self.ks[b, g])
+                    if self.v is not None:
+                        self.v[b, g] = self._q(self.v[b, g], self.vs[b, g])
+        self.pos = np.asarray(lengths, np.int64).copy()
+        self.nt = np.asarray(res.n_topk).copy()
+
+    @staticmethod
+    def _q(x, sc):
+        return oracle.dequantize(oracle.quantize(x, sc), sc).reshape(x.shape)
+
+    def step(self, q, kn, vn, q_oracle=None):
+        """Append (Sec. III-C) then attend; returns [n][Hq][dv]."""
+        p = self.p
+        for b in range(len(self.pos)):
+            row = oracle.slot_of(int(self.pos[b]), p.sink, p.recent)
+            for g in range(p.n_kv_heads):
+                kr = oracle.f64(kn[b, g])
+                self.k[b, g, row] = self._q(kr, self.ks[b, g]) if self.fp8 else kr
+                if self.v is not None:
+                    vr = oracle.f64(vn[b, g])
+                    self.v[b, g, row] = self._q(vr, self.vs[b, g]) if self.fp8 else vr
+        out = oracle.decode_attn(oracle_params(p), self.pos, self.nt, q if q_oracle is None else q_oracle(q),
+                                 self.k, self.v)
+        self.pos += 1
+        return out
+
+
 def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, steps, out_dtype, tol,
-                 check_every=1, layer=0, salt=0, fused=False, q_oracle=None, stats=None):
+                 check_every=1, layer=0, salt=0, fused=False, q_oracle=None, stats=None, e2e=None):
     """Run `steps` decode steps (append, attend, advance) and check each checked
     step against the oracle on the GPU's cache.  Returns the max abs error.
-    fused: append and attend through snap_decode_step instead of two calls.
+    fused: append and attend through snap_decode_step instead of two calls
+    ("alt": two calls on even steps, the fused step on odd ones).
     q_oracle: the query the oracle attends with (e.g. fp8_query); stats, if a
-    dict, gets the max abs deviation from the oracle on the exact query."""
+    dict, gets the max abs deviation from the oracle on the exact query, and
+    with e2e (an OracleCache of the same sequences, stepped every step) the
+    end-to-end error "e2e_err": GPU output against the oracle's decode over the
+    oracle's own cache."""
     dev = cache.k.device
     sl = torch.tensor(slots, dtype=torch.int32, device=dev)
     n = len(slots)
@@ -198,8 +313,10 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
         q, kn, vn = synth.decode_inputs(wl, layer, step, positions, salt=salt)
         check = (step % check_every == 0) or step == steps - 1
         if check:
-            before_k, before_v = cache.host_values()
-        if fused:
+            before_k = raw(cache.k).clone()
+            before_v = None if cache.v is None else raw(cache.v).clone()
+        use_fused = fused if fused != "alt" else bool(step & 1)
+        if use_fused:
             snap.snap_decode_step(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), kn.to(dev),
                                   None if vn is None else vn.to(dev), out, ws)
         else:
@@ -207,16 +324,21 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
             snap.snap_decode_attn(p, cache.c(), cache.pos, cache.n_topk, sl, q.to(dev), out, ws)
         snap.snap_advance(cache.pos, sl)
         torch.cuda.synchronize()
+        exp_e2e = None if e2e is None else e2e.step(q, kn, vn, q_oracle)
         if not check:
             continue
         ck, cv = cache.host_values()
         nt = cache.n_topk.cpu().numpy()
         # the append touched exactly one row per (slot, head): the ring row of the position
+        after_k = raw(cache.k)
+        after_v = None if cache.v is None else raw(cache.v)
         for i, s_ in enumerate(slots):
             row = oracle.slot_of(positions[i], p.sink, p.recent)
-            mask = np.ones(ck.shape[2], bool)
+            mask = torch.ones(cache.k.shape[2], dtype=torch.bool, device=dev)
             mask[row] = False
-            assert np.array_equal(ck[s_][:, mask], before_k[s_][:, mask]), "append wrote outside its row"
+            assert torch.equal(after_k[s_][:, mask], before_k[s_][:, mask]), "append wrote outside its row"
+            if after_v is not None:
+                assert torch.equal(after_v[s_][:, mask], before_v[s_][:, mask]), "append wrote outside its row"
             if p.kv_dtype != snap.SNAP_FP8_E4M3:
                 assert np.array_equal(ck[s_][:, row], oracle.f64(kn[i])), "appended K row"
                 if cv is not None:
@@ -224,7 +346,10 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
             else:
                 for g in range(p.n_kv_heads):
                     codes = oracle.quantize(oracle.f64(kn[i, g]), float(cache.k_scale[s_, g]))
-                    assert np.array_equal(cache.k[s_, g, row].cpu().numpy(), codes)
+                    assert np.array_equal(cache.k[s_, g, row].cpu().numpy(), codes), "appended K codes"
+                    if cache.v is not None:
+                        codes = oracle.quantize(oracle.f64(vn[i, g]), float(cache.v_scale[s_, g]))
+                        assert np.array_equal(cache.v[s_, g, row].cpu().numpy(), codes), "appended V codes"
         cvs = None if cv is None else cv[slots]
         exp = oracle.decode_attn(op, positions, nt[slots], q if q_oracle is None else q_oracle(q), ck[slots], cvs)
         got = out.double().cpu().numpy()
@@ -232,6 +357,79 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
         if stats is not None and q_oracle is not None:
             exact = oracle.decode_attn(op, positions, nt[slots], q, ck[slots], cvs)
             stats["exact_query_dev"] = max(stats.get("exact_query_dev", 0.0), float(np.max(np.abs(got - exact))))
+        if stats is not None and exp_e2e is not None:
+            stats["e2e_err"] = max(stats.get("e2e_err", 0.0), float(np.max(np.abs(got - exp_e2e))))
         worst = max(worst, err)
         assert err <= tol, f"decode step {step}: max abs err {err}"
     return worst
+
+
+def run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
+             check_every=1, fp8_scales=False, band_rtol=None, all_rtol=None, fused=False, poison=True):
+    """Compress a padded batch into `slots` of an n_slots cache, check it
+    against the oracle (selection, pooled scores, cache bytes, untouched
+    slots), refill the rows decode must not read with the canary, then run
+    decode steps checked against the oracle on the GPU's cache, with the
+    end-to-end error (oracle cache, oracle decode) reported and held to the
+    same tolerance.  fp8_scales: the caller sets per-(slot, head) scales from
+    the prompt's amax before compressing (SNAP_FP8_SCALES_GIVEN)."""
+    q, k, v = synth.prefill_batch(wl, layer, lengths, salt=salt, pad_value=pad_value)
+    cache = GpuCache(p, n_slots)
+    given = None
+    if fp8_scales:
+        # per-(slot, head) scale = amax of the prompt rows / 448
+        for b, s_ in enumerate(slots):
+            L = lengths[b]
+            cache.k_scale[s_] = (k[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0).to(cache.k.device)
+            if v is not None:
+                cache.v_scale[s_] = (v[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6) / 448.0).to(cache.k.device)
+    sel, pooled = gpu_compress(p, cache, q, k, v, lengths, slots)
+    stats = check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
+    valid = [s_ for s_ in slots if 0 <= s_ < n_slots]
+    if p.kv_dtype == snap.SNAP_FP8_E4M3 and p.fp8_scales == snap.SNAP_FP8_SCALES_GIVEN:
+        # the scales the cache holds (the caller's): the oracle's cache uses the same
+        given = [(cache.k_scale[s_].double().cpu().numpy(),
+                  None if cache.v_scale is None else cache.v_scale[s_].double().cpu().numpy())
+                 if 0 <= s_ < n_slots else None for s_ in slots]
+    cache.assert_untouched([x for x in range(n_slots) if x not in valid])
+    print(f"  swaps within tolerance: {stats['swaps']}, pooled max rel err: {stats['pooled_rel_err']:.3e}, "
+          f"decision band: {stats['band_rel_err']:.3e}", flush=True)
+    if band_rtol is not None:
+        assert stats["band_rel_err"] <= band_rtol
+    if all_rtol is not None:
+        assert stats["pooled_rel_err"] <= all_rtol
+    err = 0.0
+    if steps:
+        if poison:
+            cache.poison_invalid_rows(valid)
+        res = stats["oracle"]
+        keep = [i for i, s_ in enumerate(slots) if 0 <= s_ < n_slots]
+        e2e = OracleCache(p, _subset(res, keep), [lengths[i] for i in keep],
+                          None if given is None else [given[i] for i in keep])
+        dstats = {}
+        err = decode_steps(p, wl, cache, valid, steps, out_dtype, tol, check_every=check_every, layer=layer,
+                           salt=salt, fused=fused, stats=dstats, e2e=e2e)
+        e2e_err = dstats.get("e2e_err", 0.0)
+        print(f"  decode max abs err over {steps} steps: {err:.3e} (same cache), {e2e_err:.3e} (end to end: "
+              f"oracle cache, oracle decode{'' if stats['swaps'] == 0 else '; index sets differ by tolerated swaps'})",
+              flush=True)
+        # with identical index sets the two caches hold the same rows: the
+        # end-to-end error then has the same bound; tolerated swaps put other
+        # tokens in a few rows, and the difference is only reported
+        if stats["swaps"] == 0:
+            assert e2e_err <= tol, f"end-to-end decode error {e2e_err}"
+        stats["e2e_err"] = e2e_err
+        cache.assert_untouched([x for x in range(n_slots) if x not in valid])
+    return stats, err
+
+
+def _subset(res, keep):
+    """The oracle's compress result restricted to the sequences `keep`."""
+    import copy
+    r = copy.copy(res)
+    r.groups = [res.groups[i] for i in keep]
+    r.cache_k = res.cache_k[keep]
+    r.cache_v = None if res.cache_v is None else res.cache_v[keep]
+    r.n_topk = np.asarray(res.n_topk)[keep]
+    r.pos = np.asarray(res.pos)[keep]
+    return r

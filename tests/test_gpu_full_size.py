@@ -145,8 +145,8 @@ def test_mla_workload_one_layer_full_size():
     _announce(f"mla-8head-61layer-b16-128k layer 0 at full size: {wl.batch} x {lengths[0]}")
     p, q, k, v, cache, sel, pooled = _compress_full(wl, lengths)
     _structural(p, k, v, cache, sel, pooled, lengths)
-    _oracle_units(p, q, k, v, cache, sel, pooled, lengths, [(5, 0)])
-    _decode_check(p, wl, cache, 2, [0, 5, 15])
+    _oracle_units(p, q, k, v, cache, sel, pooled, lengths, [(0, 0), (5, 0), (15, 0)])
+    _decode_check(p, wl, cache, 4, [0, 5, 15])
 
 
 def test_cb_fp8_workload_full_size():
@@ -190,7 +190,7 @@ def test_cb_fp8_workload_full_size():
         assert torch.all(cache.k[slots[b], :, s + r + keff:] == 0)
         assert torch.all(cache.v[slots[b], :, s + r + keff:] == 0)
     untouched = [x for x in range(wl.slots) if x not in slots]
-    assert torch.all(cache.pos[untouched] == -1)
+    cache.assert_untouched(untouched)
 
     op = oracle_params(p)
     G = op.group

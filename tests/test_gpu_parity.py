@@ -11,7 +11,8 @@ import torch
 import oracle
 import paper_2511_03092_amd as snap
 import synth
-from snaphelp import (TOL, GpuCache, check_compress, decode_steps, gpu_compress, oracle_params, params_of)
+from snaphelp import (TOL, GpuCache, check_compress, decode_steps, gpu_compress, oracle_params, params_of,
+                      run_case)
 
 pytestmark = pytest.mark.gpu
 
@@ -27,28 +28,9 @@ def _announce(msg):
     print(f"\n[case] {msg}", flush=True)
 
 
-def _run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
-              check_every=1, fp8_scales=False, band_rtol=BAND_RTOL):
-    q, k, v = synth.prefill_batch(wl, layer, lengths, salt=salt, pad_value=pad_value)
-    cache = GpuCache(p, n_slots)
-    if fp8_scales:
-        # per-(slot, head) scale = amax of the prompt rows / 448
-        for b, s_ in enumerate(slots):
-            L = lengths[b]
-            cache.k_scale[s_] = k[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6).cuda() / 448.0
-            if v is not None:
-                cache.v_scale[s_] = v[b, :, :L].float().abs().amax(dim=(1, 2)).clamp_min(1e-6).cuda() / 448.0
-    sel, pooled = gpu_compress(p, cache, q, k, v, lengths, slots)
-    stats = check_compress(p, cache, q, k, v, lengths, slots, sel, pooled)
-    print(f"  swaps within tolerance: {stats['swaps']}, pooled max rel err: {stats['pooled_rel_err']:.3e}, "
-          f"decision band: {stats['band_rel_err']:.3e}", flush=True)
-    assert stats["band_rel_err"] <= band_rtol and stats["pooled_rel_err"] <= ALL_RTOL
-    err = 0.0
-    if steps:
-        err = decode_steps(p, wl, cache, slots, steps, out_dtype, tol, check_every=check_every, layer=layer,
-                           salt=salt)
-        print(f"  decode max abs err over {steps} steps: {err:.3e}", flush=True)
-    return stats, err
+def _run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, band_rtol=BAND_RTOL, **kw):
+    return run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, band_rtol=band_rtol, all_rtol=ALL_RTOL,
+                    **kw)
 
 
 def test_tiny_fp32_workload():
