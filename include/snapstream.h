@@ -250,6 +250,28 @@ snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, cons
                              const void* q, const void* k_new, const void* v_new, void* out,
                              int32_t out_dtype, void* workspace, size_t ws_bytes, void* stream);
 
+/* Device memory of snap_decode_step_noalloc: one array of this many bytes per
+ * GPU, owned by the library. */
+#define SNAP_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* snap_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture that must not allocate, tight serving loops, harnesses
+ * that forbid allocation): the same arguments, results and cache contents,
+ * without the workspace.  The split-K partials go to a library-owned device
+ * array of SNAP_NOALLOC_SCRATCH_BYTES per GPU (reserved with the library's
+ * device code on the first call on that GPU, held until the process ends;
+ * the call itself allocates nothing).  A call that would need more than that
+ * (snap_decode_workspace(p, n) > SNAP_NOALLOC_SCRATCH_BYTES) returns
+ * SNAP_ERR_WORKSPACE and launches nothing.  Every call on one GPU shares that
+ * GPU's array: calls that may overlap in time on one GPU (other streams, or
+ * other threads without ordering between them) race and give wrong results,
+ * so serialise them.  What one call leaves in the array does not affect the
+ * next (a call writes every byte it reads first). */
+snap_status snap_decode_step_noalloc(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                                     const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
+                                     const void* k_new, const void* v_new, void* out, int32_t out_dtype,
+                                     void* stream);
+
 /* pos[slot_ids[b]] += 1 for b < n (once per decode step, after every layer).
  * pos is device int32[n_slots]; slot ids outside [0, n_slots) are skipped. */
 snap_status snap_advance(int32_t* pos, int32_t n_slots, int32_t n, const int32_t* slot_ids,

@@ -6,7 +6,8 @@ used for device memory and the current stream.  If the library is missing the
 first call raises -- there is no other implementation behind these names.
 
 Functions keep the C names (include/snapstream.h):
-    snap_compress, snap_prefill, snap_prefill_attn, snap_cache_append, snap_decode_attn, snap_decode_step, snap_advance,
+    snap_compress, snap_prefill, snap_prefill_attn, snap_cache_append, snap_decode_attn, snap_decode_step,
+    snap_decode_step_noalloc, snap_advance,
     snap_compress_workspace, snap_prefill_workspace, snap_decode_workspace, snap_status_str
 """
 from __future__ import annotations
@@ -26,7 +27,8 @@ SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
 
 EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_prefill_workspace", "snap_compress",
             "snap_prefill", "snap_prefill_attn", "snap_cache_append",
-            "snap_decode_attn", "snap_decode_step", "snap_advance", "snap_status_str", "snap_last_error"]
+            "snap_decode_attn", "snap_decode_step", "snap_decode_step_noalloc", "snap_advance", "snap_status_str",
+            "snap_last_error"]
 
 
 class SnapParams(ctypes.Structure):
@@ -80,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.snap_decode_attn.restype = ctypes.c_int
     L.snap_decode_step.argtypes = [P, C, vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]
     L.snap_decode_step.restype = ctypes.c_int
+    L.snap_decode_step_noalloc.argtypes = [P, C, vp, vp, i32, vp, vp, vp, vp, vp, i32, vp]
+    L.snap_decode_step_noalloc.restype = ctypes.c_int
     L.snap_advance.argtypes = [vp, i32, i32, vp, vp]
     L.snap_advance.restype = ctypes.c_int
     L.snap_status_str.argtypes = [ctypes.c_int]
@@ -206,6 +210,14 @@ def snap_decode_step(p: Params, cache: SnapCache, pos, n_topk, slot_ids, q, k_ne
                                   int(q.shape[0]), _ptr(slot_ids), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
                                   out_dtype, _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
+
+
+def snap_decode_step_noalloc(p: Params, cache: SnapCache, pos, n_topk, slot_ids, q, k_new, v_new, out, stream=None):
+    import torch
+    out_dtype = SNAP_BF16 if out.dtype == torch.bfloat16 else SNAP_F32
+    _check(lib().snap_decode_step_noalloc(ctypes.byref(p.c()), ctypes.byref(cache), _ptr(pos), _ptr(n_topk),
+                                          int(q.shape[0]), _ptr(slot_ids), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                          _ptr(out), out_dtype, _stream(stream)))
 
 
 def snap_advance(pos, slot_ids, stream=None):

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsnapstream.so")
-SOURCES = ["abi.hip", "compress.hip", "decode.hip", "prefill.hip"]
+SOURCES = ["abi.hip", "compress.hip", "decode.hip", "prefill.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

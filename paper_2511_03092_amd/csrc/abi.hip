@@ -1,6 +1,8 @@
 // abi.hip -- the extern "C" entry points of libsnapstream: host-side argument
 // validation, workspace sizing and dispatch to the kernel launchers.  Nothing
-// here allocates device memory, synchronises or queries the device, so every
+// here allocates device memory or synchronises, and every validation runs
+// before anything touches the device (the one device query, of
+// snap_decode_step_noalloc's scratch address, follows its checks), so every
 // validation path can run on a host without a GPU.
 #include <math.h>
 #include <stdarg.h>
@@ -254,11 +256,11 @@ snap_status snap_decode_attn(const snap_params* p, const snap_cache* cache, cons
   return st;
 }
 
-snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
-                             const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
-                             const void* k_new, const void* v_new, void* out, int32_t out_dtype, void* workspace,
-                             size_t ws_bytes, void* stream) {
-  g_err[0] = 0;
+// Checks of snap_decode_step and snap_decode_step_noalloc except the
+// workspace.
+static snap_status check_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                                     const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
+                                     const void* k_new, const void* v_new, void* out, int32_t out_dtype) {
   snap_status st = check_params(p);
   if (st != SNAP_OK) return st;
   if ((st = check_cache(p, cache)) != SNAP_OK) return st;
@@ -273,11 +275,40 @@ snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, cons
     return fail(SNAP_ERR_INVALID_ARG, "v_new is NULL or not 16-byte aligned");
   if (!out || !aligned16(out)) return fail(SNAP_ERR_INVALID_ARG, "out is NULL or not 16-byte aligned");
   if (out_dtype != SNAP_F32 && out_dtype != SNAP_BF16) return fail(SNAP_ERR_INVALID_ARG, "out_dtype must be F32 or BF16");
+  return SNAP_OK;
+}
+
+snap_status snap_decode_step(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                             const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
+                             const void* k_new, const void* v_new, void* out, int32_t out_dtype, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  snap_status st = check_decode_step(p, cache, pos, n_topk, n, slot_ids, q, k_new, v_new, out, out_dtype);
+  if (st != SNAP_OK || n == 0) return st;
   const size_t need = decode_geometry(*p, n).decode_bytes;
   if (!workspace || ((uintptr_t)workspace & 255u) || ws_bytes < need)
     return fail(SNAP_ERR_WORKSPACE, "workspace needs %zu bytes, 256-byte aligned (got %zu)", need, ws_bytes);
   st = launch_decode(*p, *cache, pos, n_topk, n, slot_ids, q, k_new, p->v_in_k ? nullptr : v_new, out, out_dtype,
                      workspace, (hipStream_t)stream);
+  if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return st;
+}
+
+snap_status snap_decode_step_noalloc(const snap_params* p, const snap_cache* cache, const int32_t* pos,
+                                     const int32_t* n_topk, int32_t n, const int32_t* slot_ids, const void* q,
+                                     const void* k_new, const void* v_new, void* out, int32_t out_dtype,
+                                     void* stream) {
+  g_err[0] = 0;
+  snap_status st = check_decode_step(p, cache, pos, n_topk, n, slot_ids, q, k_new, v_new, out, out_dtype);
+  if (st != SNAP_OK || n == 0) return st;
+  const size_t need = decode_geometry(*p, n).decode_bytes;
+  if (need > (size_t)SNAP_NOALLOC_SCRATCH_BYTES)
+    return fail(SNAP_ERR_WORKSPACE, "this call needs %zu bytes of scratch; the library's array holds %zu (split the batch)",
+                need, (size_t)SNAP_NOALLOC_SCRATCH_BYTES);
+  void* scratch = nullptr;
+  if ((st = noalloc_scratch(&scratch)) != SNAP_OK) return st;
+  st = launch_decode(*p, *cache, pos, n_topk, n, slot_ids, q, k_new, p->v_in_k ? nullptr : v_new, out, out_dtype,
+                     scratch, (hipStream_t)stream);
   if (st == SNAP_ERR_HIP) set_error("kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
   return st;
 }

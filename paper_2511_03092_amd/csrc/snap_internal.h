@@ -162,6 +162,9 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
                           hipStream_t stream);
 snap_status launch_advance(int32_t* pos, int n_slots, int n, const int32_t* slot_ids, hipStream_t stream);
 
+// device address of the current GPU's snap_decode_step_noalloc scratch array
+snap_status noalloc_scratch(void** addr);
+
 void set_error(const char* fmt, ...);
 
 }  // namespace snap

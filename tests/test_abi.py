@@ -162,6 +162,32 @@ def test_decode_step_validation():
     assert b"workspace" in snap.lib().snap_last_error()
 
 
+def test_noalloc_step_validation():
+    """snap_decode_step_noalloc makes snap_decode_step's checks and refuses a
+    call whose partials would not fit the library's scratch array, before any
+    device query (so on a host without a GPU)."""
+    L = snap.lib()
+    p = _params()
+    cache = snap.SnapCache(FAKE, FAKE, None, None, 4)
+
+    def step(n=2, params=p, c=cache, v_new=FAKE, out_dtype=snap.SNAP_BF16):
+        return L.snap_decode_step_noalloc(ctypes.byref(params.c()), ctypes.byref(c), FAKE, FAKE, n, FAKE, FAKE,
+                                          FAKE, v_new, FAKE, out_dtype, None)
+
+    assert step(v_new=None) == snap.SNAP_ERR_INVALID_ARG
+    assert step(out_dtype=snap.SNAP_FP8_E4M3) == snap.SNAP_ERR_INVALID_ARG
+    assert step(n=0) == snap.SNAP_OK
+    assert step(params=_params(pool_kernel=4)) == snap.SNAP_ERR_INVALID_ARG
+    # latent rows (512 value dims) for 8191 sequences of 8 heads: one chunk
+    # each, 8191 * 8 * 512 * 4 bytes of partials > the 32 MiB array
+    lat = _params(n_q_heads=8, n_kv_heads=1, d_qk=576, d_v=512, v_in_k=1, recent=4096, topk=28668)
+    lcache = snap.SnapCache(FAKE, None, None, None, 4)
+    n = 8191
+    assert snap.snap_decode_workspace(lat, n) > (32 << 20)
+    assert step(n=n, params=lat, c=lcache, v_new=None) == snap.SNAP_ERR_WORKSPACE
+    assert b"scratch" in L.snap_last_error()
+
+
 def test_prefill_validation():
     """snap_prefill: the shapes it supports, its workspace and pointer checks,
     all before any launch."""
