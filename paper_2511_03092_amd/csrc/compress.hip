@@ -441,6 +441,8 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
 struct ReduceArgs {
   const float2* stats;
   float2* rowref;
+  double2* rowz;       // [groups][rows_pad] (max in log2 units, sum of 2^(y - max)) in fp64
+  int32_t* band_n;     // [groups] members of the re-score band (reset here)
   const int32_t* lengths;
   uint32_t* hist;      // [3][groups][kRadixBins]
   RadixState* state;   // [groups]
@@ -489,9 +491,11 @@ __global__ __launch_bounds__(256) void stats_reduce(ReduceArgs a) {
         }
       }
       a.rowref[(size_t)bg * a.rows_pad + rho] = ref;
+      a.rowz[(size_t)bg * a.rows_pad + rho] = make_double2((double)m, z);
     }
   }
   if (bid_x() != 0) return;
+  if (tid() == 0) a.band_n[bg] = 0;
   for (int pass = 0; pass < 3; ++pass) {
     uint32_t* h = a.hist + ((size_t)pass * a.groups + bg) * kRadixBins;
     for (int i = tid(); i < kRadixBins; i += nthreads()) h[i] = 0u;
@@ -523,8 +527,22 @@ struct SelectArgs {
   RadixState* state;     // [groups]
   uint2* counts;         // [groups][n_splits] (greater, equal)
   int32_t* sel;          // [groups][topk]
+  int32_t* band_n;       // [groups] candidates in the re-score band
+  int32_t* band_idx;     // [groups][kBandCap] their token indices (in arrival order)
+  uint32_t* band_above;  // [groups][n_splits] candidates above the band per split
   int groups, Hkv, max_len, sink, recent, topk, pool_kernel, pool, n_splits;
 };
+
+// The re-score band around the K-th largest pooled score tau (fp32 bits of a
+// non-negative value): [tau (1 - 2^-14), tau (1 + 2^-14)] as bit patterns.
+// The fp32 score path is accurate to a few 1e-6 relative, so no candidate
+// outside the band can be on the other side of the threshold.
+constexpr float kBandRel = 1.0f / 16384.0f;
+__device__ __forceinline__ void band_limits(uint32_t tau_bits, uint32_t& lo, uint32_t& hi) {
+  const float t = __uint_as_float(tau_bits);
+  lo = __float_as_uint(t * (1.0f - kBandRel));
+  hi = __float_as_uint(t * (1.0f + kBandRel));
+}
 
 // the group's selection state, with every field in scalar registers
 __device__ __forceinline__ RadixState load_state(const RadixState* p) {
@@ -712,16 +730,189 @@ __global__ __launch_bounds__(kSelThreads) void select_count(SelectArgs a) {
   seq_range(a, bg, c0, c1);
   const int j0 = c0 + split * kCandChunk, j1 = min(j0 + kCandChunk, c1);
   const float* Pg = a.P + (size_t)bg * a.max_len;
-  uint32_t gt = 0, eq = 0;
+  uint32_t lo, hi;
+  band_limits(st.prefix, lo, hi);
+  uint32_t gt = 0, eq = 0, above = 0;
   for (int j = j0 + tid(); j < j1; j += nthreads()) {
     uint32_t bits = __float_as_uint(Pg[j]);
     gt += bits > st.prefix;
     eq += bits == st.prefix;
+    above += bits > hi;
+    if (bits >= lo && bits <= hi) {
+      const int m = atomicAdd(&a.band_n[bg], 1);
+      if (m < kBandCap) a.band_idx[(size_t)bg * kBandCap + m] = j;
+    }
   }
-  uint32_t tg, te;
+  uint32_t tg, te, ta;
   block_exclusive_scan(gt, lds, tg);
   block_exclusive_scan(eq, lds, te);
-  if (tid() == 0) a.counts[(size_t)bg * a.n_splits + split] = make_uint2(tg, te);
+  block_exclusive_scan(above, lds, ta);
+  if (tid() == 0) {
+    a.counts[(size_t)bg * a.n_splits + split] = make_uint2(tg, te);
+    a.band_above[(size_t)bg * a.n_splits + split] = ta;
+  }
+}
+
+// ============================================================ fp64 re-score of the band
+// Every candidate in the band gets its pooled score again in fp64 (Eq. 1-3
+// with exact products of the bf16 / fp32 inputs, fp64 exponentials and the
+// rows' fp64 normalisers), so the selection near the threshold does not rest
+// on the fp32 logits of the score passes.  One workgroup per band member at a
+// time (members strided over the grid); thread rho owns score row rho.
+struct BandArgs {
+  const void* q;          // [n_seq][Hq][w][D]
+  const void* k;          // [n_seq][Hkv][max_len][D]
+  const int32_t* lengths;
+  const double2* rowz;    // [groups][rows_pad]
+  const RadixState* state;
+  const int32_t* band_n;
+  const int32_t* band_idx;
+  double* band_p;         // [groups][kBandCap] fp64 pooled scores of the members
+  float* pooled_out;      // optional debug copy: the members' re-scored values
+  float* P;               // [groups][max_len]
+  uint2* counts;          // [groups][n_splits]
+  const uint32_t* band_above;
+  RadixState* state_w;
+  int Hq, Hkv, G, w, D, max_len, sink, recent, pool_kernel, pool, rows, rows_pad, n_splits, in_f32;
+  int band_wgs;           // workgroups per group of band_rescore (members strided over them)
+  double scale2;          // sm_scale * log2(e) in fp64
+};
+
+__device__ __forceinline__ double block_sum_f64(double v, double* lds) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  __syncthreads();
+  if ((tid() & 63) == 0) lds[tid() >> 6] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int i = 0; i < (int)(nthreads() >> 6); ++i) s += lds[i];
+  return s;
+}
+
+constexpr int kBandWGs = 32;  // band_rescore workgroups per group (members strided over them)
+__global__ __launch_bounds__(256) void band_rescore(BandArgs a) {
+  __shared__ double lds[4];
+  const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
+  const RadixState st = load_state(&a.state[bg]);
+  if (st.mode != 2) return;
+  const int nb = uniform(a.band_n[bg]);
+  if (nb > kBandCap) return;  // too many: the fp32 selection stands
+  int L = uniform(a.lengths[b]);
+  L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
+  const int c0 = a.sink, c1 = L - a.recent;
+  const int half = a.pool_kernel / 2;
+  const int we = min(a.w, L);
+  // this thread's score row
+  const int rho = tid();
+  const int ii = rho % a.w;
+  const bool rval = rho < a.rows && ii >= a.w - we;
+  const int rpos = L - a.w + ii;
+  const double2 nz = rval ? a.rowz[(size_t)bg * a.rows_pad + rho] : make_double2(0.0, 0.0);
+  const bool live = rval && nz.y > 0.0;
+  const size_t qoff = (((size_t)b * a.Hq + (size_t)g * a.G) * a.w + (rho < a.rows ? rho : 0)) * a.D;
+  const size_t krow0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
+  for (int m = bid_x(); m < nb; m += a.band_wgs) {
+    const int j = a.band_idx[(size_t)bg * kBandCap + m];
+    const int t0 = max(j - half, c0), t1 = min(j + half, c1 - 1);
+    double pooled = a.pool == SNAP_POOL_MAX ? -1.0 : 0.0;
+    for (int t = t0; t <= t1; ++t) {
+      double wgt = 0.0;
+      if (live && t <= rpos) {
+        double dot = 0.0;
+        if (a.in_f32) {
+          const float* qr = (const float*)a.q + qoff;
+          const float* kr = (const float*)a.k + (krow0 + t) * a.D;
+          for (int d = 0; d < a.D; ++d) dot = fma((double)qr[d], (double)kr[d], dot);
+        } else {
+          const uint16_t* qr = (const uint16_t*)a.q + qoff;
+          const uint16_t* kr = (const uint16_t*)a.k + (krow0 + t) * a.D;
+          for (int d = 0; d < a.D; d += 8) {
+            const u32x4 qv = *(const u32x4*)(qr + d), kv = *(const u32x4*)(kr + d);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              dot = fma((double)bf16_bits_to_f32(qv[e] & 0xffffu), (double)bf16_bits_to_f32(kv[e] & 0xffffu), dot);
+              dot = fma((double)bf16_bits_to_f32(qv[e] >> 16), (double)bf16_bits_to_f32(kv[e] >> 16), dot);
+            }
+          }
+        }
+        wgt = exp2(dot * a.scale2 - nz.x) / nz.y;
+      }
+      const double At = block_sum_f64(wgt, lds);
+      if (a.pool == SNAP_POOL_MAX)
+        pooled = At > pooled ? At : pooled;
+      else
+        pooled += At;
+    }
+    if (tid() == 0) {
+      if (a.pool != SNAP_POOL_MAX) pooled /= (double)a.pool_kernel;
+      a.band_p[(size_t)bg * kBandCap + m] = pooled;
+      if (a.pooled_out) a.pooled_out[(size_t)bg * a.max_len + j] = (float)pooled;
+    }
+  }
+}
+
+// One workgroup per group: rank the band members by (fp64 pooled score
+// descending, token index ascending), keep as many as the K_eff - (members
+// above the band) places left, and rewrite the members' P so that the
+// ordered compaction keeps exactly the candidates above the band and the kept
+// members: P > hi for kept ones, 0 for the others, threshold hi, no ties.
+__global__ __launch_bounds__(kSelThreads) void band_decide(BandArgs a) {
+  __shared__ double sp[kBandCap];
+  __shared__ int32_t sj[kBandCap];
+  __shared__ uint32_t lds[8];
+  const int bg = bid_x();
+  RadixState st = load_state(&a.state[bg]);
+  if (st.mode != 2) return;
+  const int nb = uniform(a.band_n[bg]);
+  if (nb > kBandCap) return;
+  uint32_t lo, hi;
+  band_limits(st.prefix, lo, hi);
+  // members above the band (all kept)
+  uint32_t above = 0;
+  for (int s = tid(); s < a.n_splits; s += nthreads()) above += a.band_above[(size_t)bg * a.n_splits + s];
+  uint32_t n_above;
+  block_exclusive_scan(above, lds, n_above);
+  const int need = st.keff - (int)n_above;  // in [1, nb] (tau itself is a member)
+  if (need < 0 || need > nb) return;         // not for finite scores; the fp32 selection stands
+  for (int i = tid(); i < kBandCap; i += nthreads()) {
+    sp[i] = i < nb ? a.band_p[(size_t)bg * kBandCap + i] : -2.0;   // pads sort last
+    sj[i] = i < nb ? a.band_idx[(size_t)bg * kBandCap + i] : 0x7fffffff;
+  }
+  __syncthreads();
+  // bitonic sort of kBandCap entries, first = (score desc, index asc)
+  for (int size = 2; size <= kBandCap; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid(); i < kBandCap; i += nthreads()) {
+        const int jx = i ^ stride;
+        if (jx > i) {
+          const bool asc = (i & size) == 0;  // this pair sorts "first before second"
+          const double pi = sp[i], pj = sp[jx];
+          const int ji = sj[i], jj = sj[jx];
+          const bool i_first = pi > pj || (pi == pj && ji < jj);
+          if (asc != i_first) {
+            sp[i] = pj; sp[jx] = pi;
+            sj[i] = jj; sj[jx] = ji;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // per-split counts of what the compaction keeps: the candidates above the
+  // band and the kept members
+  const int c0 = a.sink;
+  for (int s = tid(); s < a.n_splits; s += nthreads()) {
+    uint32_t n = a.band_above[(size_t)bg * a.n_splits + s];
+    for (int i = 0; i < need; ++i) n += (sj[i] - c0) / kCandChunk == s;
+    a.counts[(size_t)bg * a.n_splits + s] = make_uint2(n, 0u);
+  }
+  float* Pg = a.P + (size_t)bg * a.max_len;
+  for (int i = tid(); i < nb; i += nthreads()) Pg[sj[i]] = __uint_as_float(i < need ? hi + 1u : 0u);
+  if (tid() == 0) {
+    st.prefix = hi;
+    st.krem = 0;
+    a.state_w[bg] = st;
+  }
 }
 
 // Ordered compaction: a candidate is kept when P > t, or P == t and it is among
@@ -1097,6 +1288,16 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   g.n_rowblocks = (p.sink + p.recent + p.topk + kAsmRows - 1) / kAsmRows;
   g.off_amax = off;
   off = align256(off + (size_t)groups * g.n_rowblocks * sizeof(float2));
+  g.off_rowz = off;
+  off = align256(off + (size_t)groups * g.rows_pad * sizeof(double2));
+  g.off_band_n = off;
+  off = align256(off + (size_t)groups * sizeof(int32_t));
+  g.off_band_idx = off;
+  off = align256(off + (size_t)groups * kBandCap * sizeof(int32_t));
+  g.off_band_p = off;
+  off = align256(off + (size_t)groups * kBandCap * sizeof(double));
+  g.off_band_above = off;
+  off = align256(off + (size_t)groups * g.n_splits * sizeof(uint32_t));
   g.compress_bytes = off;
   return g;
 }
@@ -1152,6 +1353,11 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   RadixState* state = (RadixState*)(w + geo.off_state);
   uint2* counts = (uint2*)(w + geo.off_counts);
   int32_t* sel = (int32_t*)(w + geo.off_sel);
+  double2* rowz = (double2*)(w + geo.off_rowz);
+  int32_t* band_n = (int32_t*)(w + geo.off_band_n);
+  int32_t* band_idx = (int32_t*)(w + geo.off_band_idx);
+  double* band_p = (double*)(w + geo.off_band_p);
+  uint32_t* band_above = (uint32_t*)(w + geo.off_band_above);
 
   ScoreArgs sa;
   sa.q = q_obs;
@@ -1194,6 +1400,8 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
     ReduceArgs ra;
     ra.stats = stats;
     ra.rowref = rowref;
+    ra.rowz = rowz;
+    ra.band_n = band_n;
     ra.lengths = lengths;
     ra.hist = hist;
     ra.state = state;
@@ -1222,6 +1430,9 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
     se.state = state;
     se.counts = counts;
     se.sel = sel;
+    se.band_n = band_n;
+    se.band_idx = band_idx;
+    se.band_above = band_above;
     se.groups = groups;
     se.Hkv = p.n_kv_heads;
     se.max_len = max_len;
@@ -1239,6 +1450,40 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
     hipLaunchKernelGGL(radix_pass, sgrid, dim3(kSelThreads), 0, stream, se, 2);
     hipLaunchKernelGGL(radix_scan, dim3(groups), dim3(kSelThreads), 0, stream, se, 2);
     hipLaunchKernelGGL(select_count, sgrid, dim3(kSelThreads), 0, stream, se);
+    // fp64 re-score of the candidates next to the threshold, then the final
+    // decision among them
+    BandArgs ba;
+    ba.q = q_obs;
+    ba.k = k;
+    ba.lengths = lengths;
+    ba.rowz = rowz;
+    ba.state = state;
+    ba.band_n = band_n;
+    ba.band_idx = band_idx;
+    ba.band_p = band_p;
+    ba.pooled_out = pooled_out;
+    ba.P = P;
+    ba.counts = counts;
+    ba.band_above = band_above;
+    ba.state_w = state;
+    ba.Hq = p.n_q_heads;
+    ba.Hkv = p.n_kv_heads;
+    ba.G = G;
+    ba.w = p.obs_window;
+    ba.D = p.d_qk;
+    ba.max_len = max_len;
+    ba.sink = p.sink;
+    ba.recent = p.recent;
+    ba.pool_kernel = p.pool_kernel;
+    ba.pool = p.pool;
+    ba.rows = geo.rows;
+    ba.rows_pad = geo.rows_pad;
+    ba.n_splits = geo.n_splits;
+    ba.in_f32 = !bf;
+    ba.band_wgs = kBandWGs;
+    ba.scale2 = (double)scale * 1.4426950408889634074;
+    hipLaunchKernelGGL(band_rescore, dim3(kBandWGs, groups), dim3(256), 0, stream, ba);
+    hipLaunchKernelGGL(band_decide, dim3(groups), dim3(kSelThreads), 0, stream, ba);
     hipLaunchKernelGGL(select_write, sgrid, dim3(kSelThreads), 0, stream, se);
     if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
   }

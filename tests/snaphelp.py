@@ -20,6 +20,43 @@ import synth
 
 SEL_RTOL = 1e-6
 TOL = {"f32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
+
+# Pooled-score accuracy against the oracle (relative):
+#  * decision band -- candidates within 2^-15 of the K-th largest score, the
+#    ones the selection decides among: the library re-scores every candidate
+#    within 2^-14 of its own threshold in fp64, so what remains is the fp32
+#    rounding of the stored score (6e-8) and the error of the rows'
+#    normalisers, which sum exponentials of fp32 logits: a row dominated by one
+#    large logit y carries up to about ln2 * |y| * 2^-23 (~1e-6 at y = 17) in
+#    its normaliser, and a candidate's score averages that over the rows that
+#    weigh it (measured at most 2.9e-7, on 32-row windows);
+#  * near band -- within a factor 4 of it (fp32 score path: exp2 to 1 ulp,
+#    fp32 logits from the MFMA accumulation, the column-sum and pooling trees;
+#    ~1e-6 with w = 32, ~3e-6 with one window row, where a key's score sums
+#    only G weights);
+#  * anywhere -- large planted logits carry the most fp32 rounding.
+DECISION_RTOL = 5e-7
+DECISION_RTOL_BAND = 2.0 ** -15
+NEAR_RTOL = 1e-6
+NEAR_RTOL_ONE_ROW = 3e-6
+ALL_RTOL = 1e-5
+
+
+def score_errors(gp, P, keff):
+    """Relative errors of the GPU pooled scores gp against the oracle's P over
+    one group's candidates (both [n_cand]): anywhere, in the near band and in
+    the decision band (zeros when nothing is decided: keff 0 or all kept)."""
+    gp = np.asarray(gp, np.float64)
+    P = np.asarray(P, np.float64)
+    rel = np.abs(gp - P) / np.maximum(np.abs(P), 1e-30)
+    out = dict(all=float(rel.max()) if rel.size else 0.0, near=0.0, decision=0.0)
+    if 0 < keff < P.size:
+        tau = np.sort(P)[::-1][keff - 1]
+        near = (P >= tau / 4) & (P <= tau * 4)
+        dec = np.abs(P / tau - 1.0) <= DECISION_RTOL_BAND
+        out["near"] = float(rel[near].max())
+        out["decision"] = float(rel[dec].max())
+    return out
 DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
 
 
@@ -169,9 +206,9 @@ def expected_cache(L, s, r, K, x, sel):
 
 
 def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gsel, gpooled):
-    """Full check of one compress call.  Returns the tolerated swaps, the max
-    relative error of the pooled scores over all candidates, and over the
-    decision band (oracle score within a factor 4 of the K-th largest)."""
+    """Full check of one compress call.  Returns the tolerated swaps and the max
+    relative errors of the pooled scores over all candidates, the near band and
+    the decision band (see score_errors)."""
     op = oracle_params(p)
     res = oracle.compress(op, lengths, q, k, v)
     ck, cv = cache.host_values()
@@ -179,7 +216,7 @@ def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gse
     nt = cache.n_topk.cpu().numpy()
     kin = oracle.f64(k)
     vin = None if v is None else oracle.f64(v)
-    swaps, rel, band_rel = 0, 0.0, 0.0
+    swaps, rel, near_rel, dec_rel = 0, 0.0, 0.0, 0.0
     for b, L in enumerate(lengths):
         sl = slots[b]
         if sl < 0 or sl >= cache.n_slots:
@@ -190,16 +227,8 @@ def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gse
             c0, c1 = p.sink, L - p.recent
             if c1 > c0:
                 P = gr.P
-                gp = gpooled[b, g, c0:c1].astype(np.float64)
-                denom = np.maximum(np.abs(P[c0:c1]), 1e-30)
-                relv = np.abs(gp - P[c0:c1]) / denom
-                rel = max(rel, float(np.max(relv)))
-                keff_g = min(p.topk, c1 - c0)
-                if 0 < keff_g < c1 - c0:
-                    # decision band: candidates within a factor 4 of the K-th score
-                    tau = np.sort(P[c0:c1])[::-1][keff_g - 1]
-                    band = (P[c0:c1] >= tau / 4) & (P[c0:c1] <= tau * 4)
-                    band_rel = max(band_rel, float(np.max(relv[band])))
+                e = score_errors(gpooled[b, g, c0:c1], P[c0:c1], min(p.topk, c1 - c0))
+                rel, near_rel, dec_rel = max(rel, e["all"]), max(near_rel, e["near"]), max(dec_rel, e["decision"])
                 assert np.all(np.isnan(gpooled[b, g, :c0])) and np.all(np.isnan(gpooled[b, g, c1:L]))
                 swaps += check_selection(gsel[b, g], P, L, p.sink, p.recent, p.topk)
             else:
@@ -221,7 +250,7 @@ def check_compress(p: snap.Params, cache: GpuCache, q, k, v, lengths, slots, gse
                     assert np.array_equal(cache.v[sl, g].cpu().numpy(), codes), "fp8 V codes"
                 else:
                     assert np.array_equal(cv[sl, g], ev), f"V cache rows (seq {b}, head {g})"
-    return dict(swaps=swaps, pooled_rel_err=rel, band_rel_err=band_rel, oracle=res)
+    return dict(swaps=swaps, pooled_rel_err=rel, near_rel_err=near_rel, decision_rel_err=dec_rel, oracle=res)
 
 
 def fp8_query(q) -> np.ndarray:
@@ -365,7 +394,7 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
 
 
 def run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
-             check_every=1, fp8_scales=False, band_rtol=None, all_rtol=None, fused=False, poison=True):
+             check_every=1, fp8_scales=False, near_rtol=NEAR_RTOL, all_rtol=ALL_RTOL, fused=False, poison=True):
     """Compress a padded batch into `slots` of an n_slots cache, check it
     against the oracle (selection, pooled scores, cache bytes, untouched
     slots), refill the rows decode must not read with the canary, then run
@@ -392,12 +421,12 @@ def run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=fl
                   None if cache.v_scale is None else cache.v_scale[s_].double().cpu().numpy())
                  if 0 <= s_ < n_slots else None for s_ in slots]
     cache.assert_untouched([x for x in range(n_slots) if x not in valid])
-    print(f"  swaps within tolerance: {stats['swaps']}, pooled max rel err: {stats['pooled_rel_err']:.3e}, "
-          f"decision band: {stats['band_rel_err']:.3e}", flush=True)
-    if band_rtol is not None:
-        assert stats["band_rel_err"] <= band_rtol
-    if all_rtol is not None:
-        assert stats["pooled_rel_err"] <= all_rtol
+    print(f"  swaps within tolerance: {stats['swaps']}; pooled-score rel err: decision band "
+          f"{stats['decision_rel_err']:.3e}, near band {stats['near_rel_err']:.3e}, anywhere "
+          f"{stats['pooled_rel_err']:.3e}", flush=True)
+    assert stats["decision_rel_err"] <= DECISION_RTOL
+    assert stats["near_rel_err"] <= near_rtol
+    assert stats["pooled_rel_err"] <= all_rtol
     err = 0.0
     if steps:
         if poison:
