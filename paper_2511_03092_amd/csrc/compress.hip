@@ -534,10 +534,11 @@ struct SelectArgs {
 };
 
 // The re-score band around the K-th largest pooled score tau (fp32 bits of a
-// non-negative value): [tau (1 - 2^-14), tau (1 + 2^-14)] as bit patterns.
-// The fp32 score path is accurate to a few 1e-6 relative, so no candidate
-// outside the band can be on the other side of the threshold.
-constexpr float kBandRel = 1.0f / 16384.0f;
+// non-negative value): [tau (1 - 2^-17), tau (1 + 2^-17)] as bit patterns.
+// The fp32 score path is accurate to under 2e-6 relative (measured up to
+// 1.6e-6 anywhere, 1.2e-6 near the threshold with one window row), so a
+// candidate outside the band cannot be on the other side of the threshold.
+constexpr float kBandRel = 1.0f / 131072.0f;
 __device__ __forceinline__ void band_limits(uint32_t tau_bits, uint32_t& lo, uint32_t& hi) {
   const float t = __uint_as_float(tau_bits);
   lo = __float_as_uint(t * (1.0f - kBandRel));
@@ -697,7 +698,7 @@ __global__ __launch_bounds__(kSelThreads) void radix_scan(SelectArgs a, int pass
   }
 }
 
-// block-wide exclusive scan of one value per thread (kSelThreads threads)
+// block-wide exclusive scan of one value per thread (lds holds one value per wave)
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& total) {
   const int lane = tid() & 63, wave = tid() >> 6;
   uint32_t x = v;
@@ -710,7 +711,7 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds, uint32_t& to
   __syncthreads();
   uint32_t base = 0;
   total = 0;
-  for (int w2 = 0; w2 < kSelThreads / 64; ++w2) {
+  for (int w2 = 0; w2 < (int)(nthreads() >> 6); ++w2) {
     uint32_t t = lds[w2];
     if (w2 < wave) base += t;
     total += t;
@@ -757,8 +758,11 @@ __global__ __launch_bounds__(kSelThreads) void select_count(SelectArgs a) {
 // Every candidate in the band gets its pooled score again in fp64 (Eq. 1-3
 // with exact products of the bf16 / fp32 inputs, fp64 exponentials and the
 // rows' fp64 normalisers), so the selection near the threshold does not rest
-// on the fp32 logits of the score passes.  One workgroup per band member at a
-// time (members strided over the grid); thread rho owns score row rho.
+// on the fp32 logits of the score passes.  band_rescore forms the summed
+// attention A of every key in the members' pooling windows, once per key:
+// with the members sorted by token, member m owns the keys of its window
+// past the previous member's window.  band_decide then pools, ranks and
+// decides.
 struct BandArgs {
   const void* q;          // [n_seq][Hq][w][D]
   const void* k;          // [n_seq][Hkv][max_len][D]
@@ -767,6 +771,7 @@ struct BandArgs {
   const RadixState* state;
   const int32_t* band_n;
   const int32_t* band_idx;
+  double* A64;            // [groups][max_len] fp64 A of the window keys
   double* band_p;         // [groups][kBandCap] fp64 pooled scores of the members
   float* pooled_out;      // optional debug copy: the members' re-scored values
   float* P;               // [groups][max_len]
@@ -774,140 +779,269 @@ struct BandArgs {
   const uint32_t* band_above;
   RadixState* state_w;
   int Hq, Hkv, G, w, D, max_len, sink, recent, pool_kernel, pool, rows, rows_pad, n_splits, in_f32;
-  int band_wgs;           // workgroups per group of band_rescore (members strided over them)
+  int band_wgs;           // workgroups per group of band_rescore (work items strided over them)
+  int rows_per_pass;      // score rows per band_rescore pass (kBandThreads / query-dim slices)
   double scale2;          // sm_scale * log2(e) in fp64
 };
 
-__device__ __forceinline__ double block_sum_f64(double v, double* lds) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  __syncthreads();
-  if ((tid() & 63) == 0) lds[tid() >> 6] = v;
-  __syncthreads();
-  double s = 0.0;
-  for (int i = 0; i < (int)(nthreads() >> 6); ++i) s += lds[i];
-  return s;
+// Members ranked by token index (the members are distinct): rank[i] = how
+// many members precede member i.  One pass over the list per member, no
+// barriers; nb <= kBandCap.
+__device__ __forceinline__ int token_rank(const int32_t* s, int nb, int i) {
+  const int32_t x = s[i];
+  int r = 0;
+  for (int u = 0; u < nb; ++u) r += s[u] < x;
+  return r;
 }
 
-constexpr int kBandWGs = 32;  // band_rescore workgroups per group (members strided over them)
-__global__ __launch_bounds__(256) void band_rescore(BandArgs a) {
-  __shared__ double lds[4];
+// The keys whose fp64 A the band needs, in token order: with the members
+// sorted by token, member m owns the keys of its pooling window (within the
+// candidates) that lie past the previous member's window.  Fills first[m] =
+// index of member m's first key in that order (first[nb] = the key count) and
+// tok[m] = the sorted members; returns the key count.  Every thread calls it.
+__device__ int band_keys(const int32_t* members, int nb, int half, int c0, int c1, int32_t* tok, int32_t* first,
+                         uint32_t* scan_lds) {
+  for (int i = tid(); i < nb; i += nthreads()) tok[token_rank(members, nb, i)] = members[i];
+  __syncthreads();
+  // owned key counts, then an exclusive scan over the (<= kBandCap) members
+  uint32_t total = 0;
+  for (int base = 0; base < nb; base += nthreads()) {
+    const int m = base + tid();
+    uint32_t cnt = 0;
+    if (m < nb) {
+      const int j = tok[m];
+      int t0 = max(j - half, c0);
+      if (m > 0) t0 = max(t0, tok[m - 1] + half + 1);
+      const int t1 = min(j + half, c1 - 1);
+      cnt = t1 >= t0 ? (uint32_t)(t1 - t0 + 1) : 0u;
+    }
+    uint32_t part;
+    const uint32_t ex = block_exclusive_scan(cnt, scan_lds, part);
+    if (m < nb) first[m] = (int)(total + ex);
+    total += part;
+  }
+  if (tid() == 0) first[nb] = (int)total;
+  __syncthreads();
+  return (int)total;
+}
+
+// Token of key x in the band's key order (first[] from band_keys).
+__device__ __forceinline__ int band_key_token(const int32_t* tok, const int32_t* first, int nb, int half, int c0,
+                                              int x) {
+  int lo = 0, hi = nb - 1;  // the member m with first[m] <= x < first[m+1]
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= x) lo = mid; else hi = mid - 1;
+  }
+  const int j = tok[lo];
+  int t0 = max(j - half, c0);
+  if (lo > 0) t0 = max(t0, tok[lo - 1] + half + 1);
+  return t0 + (x - first[lo]);
+}
+
+constexpr int kBandWGs = 16;       // band_rescore workgroups per group (work items strided over them)
+constexpr int kBandKeys = 4;       // keys per block (staged in LDS together)
+constexpr int kBandThreads = 512;  // rows x slices of the query dims
+constexpr int kBandKeyCap = 1024;  // band keys per group; more keeps the fp32 selection
+constexpr int kBandMaxPass = 4;    // row passes of a key block (rows_pad / rows per pass)
+// Workgroup of kBandThreads threads: thread = (score row, slice of SLICES of the
+// query dims), rows taken kBandThreads / SLICES at a time.  Each block of
+// kBandKeys keys is staged in LDS with one load round trip; the thread's
+// query slice is loaded once per block and row pass.
+template <typename In, int D, int SLICES>
+__device__ void band_rescore_body(const BandArgs& a, int bg, int b, int g, int nkeys, const int32_t* tok,
+                                  const int32_t* first, int nb, int half, int c0, int L, unsigned char* kl,
+                                  double (*red)[kBandKeys]) {
+  constexpr int kEl = 16 / (int)sizeof(In);         // elements per 16-byte chunk
+  constexpr int kRowChunks = D / kEl;
+  constexpr int CH = kRowChunks / SLICES;           // chunks per slice
+  constexpr int RPP = kBandThreads / SLICES;        // rows per pass
+  const int sl = tid() % SLICES;
+  const int we = min(a.w, L);
+  const In* qg = (const In*)a.q + ((size_t)b * a.Hq + (size_t)g * a.G) * a.w * D;
+  const size_t krow0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
+  const int lane = tid() & 63, wave = tid() >> 6;
+  const int npass = (a.rows_pad + RPP - 1) / RPP;
+  const int nblk = (nkeys + kBandKeys - 1) / kBandKeys;
+  // work items (key block, row pass), strided over the group's workgroups
+  for (int item = bid_x(); item < nblk * npass; item += a.band_wgs) {
+    const int x0 = (item / npass) * kBandKeys, r0 = (item % npass) * RPP;
+    const int nk = min(kBandKeys, nkeys - x0);
+    // stage the block's key rows (chunk c of key e at kl + (e * kRowChunks + c) * 16)
+    for (int i = tid(); i < nk * kRowChunks; i += nthreads()) {
+      const int e = i / kRowChunks, c = i % kRowChunks;
+      const int t = band_key_token(tok, first, nb, half, c0, x0 + e);
+      *((u32x4*)kl + i) = *((const u32x4*)((const In*)a.k + (krow0 + t) * D) + c);
+    }
+    int kt[kBandKeys];
+#pragma unroll
+    for (int e = 0; e < kBandKeys; ++e) kt[e] = e < nk ? band_key_token(tok, first, nb, half, c0, x0 + e) : 0;
+    // this thread's row and its query slice
+    const int rho = r0 + tid() / SLICES;
+    const int ii = rho % a.w;
+    const bool rval = rho < a.rows && ii >= a.w - we;
+    const int rpos = L - a.w + ii;
+    const double2 nz = rval ? a.rowz[(size_t)bg * a.rows_pad + rho] : make_double2(0.0, 0.0);
+    const bool live = rval && nz.y > 0.0;
+    u32x4 qv[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c)
+      qv[c] = live ? *((const u32x4*)(qg + (size_t)rho * D) + sl * CH + c) : u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < kBandKeys; ++e) {
+      double s = 0.0;
+      if (e < nk) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+          const u32x4 kv = *((const u32x4*)kl + e * kRowChunks + sl * CH + c);
+          if constexpr (sizeof(In) == 2) {
+            // a bf16 x bf16 product is exact in fp32; the sums run in fp64
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              s += (double)(bf16_bits_to_f32(qv[c][i] & 0xffffu) * bf16_bits_to_f32(kv[i] & 0xffffu));
+              s += (double)(bf16_bits_to_f32(qv[c][i] >> 16) * bf16_bits_to_f32(kv[i] >> 16));
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s = fma((double)__uint_as_float(qv[c][i]), (double)__uint_as_float(kv[i]), s);
+          }
+        }
+      }
+      // the row's dot product: sum of its slices (adjacent lanes)
+#pragma unroll
+      for (int o = 1; o < SLICES; o <<= 1) s += __shfl_xor(s, o);
+      double wv = 0.0;
+      if (sl == 0 && live && e < nk && kt[e] <= rpos) wv = exp2(s * a.scale2 - nz.x) / nz.y;
+      // summed over this pass's rows (fixed order)
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) wv += __shfl_xor(wv, o);
+      if (lane == 0) red[wave][e] = wv;
+    }
+    __syncthreads();
+    if (tid() < nk) {
+      double s = 0.0;
+      for (int w2 = 0; w2 < kBandThreads / 64; ++w2) s += red[w2][tid()];
+      a.A64[((size_t)bg * kBandKeyCap + x0 + tid()) * kBandMaxPass + item % npass] = s;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kBandThreads) void band_rescore(BandArgs a) {
+  __shared__ int32_t mem[kBandCap];
+  __shared__ int32_t tok[kBandCap];
+  __shared__ int32_t first[kBandCap + 1];
+  __shared__ uint32_t scan_lds[kBandThreads / 64];
+  __shared__ double red[kBandThreads / 64][kBandKeys];
+  __shared__ __align__(16) unsigned char kl[kBandKeys * 576 * 2];
   const int bg = bid_y(), b = bg / a.Hkv, g = bg % a.Hkv;
   const RadixState st = load_state(&a.state[bg]);
   if (st.mode != 2) return;
   const int nb = uniform(a.band_n[bg]);
   if (nb > kBandCap) return;  // too many: the fp32 selection stands
+  // at most pool_kernel keys per member, so at most this many work items:
+  // workgroups past them have nothing to do
+  if (bid_x() >= (nb * a.pool_kernel + kBandKeys - 1) / kBandKeys * kBandMaxPass) return;
   int L = uniform(a.lengths[b]);
   L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
-  const int c0 = a.sink, c1 = L - a.recent;
-  const int half = a.pool_kernel / 2;
-  const int we = min(a.w, L);
-  // this thread's score row
-  const int rho = tid();
-  const int ii = rho % a.w;
-  const bool rval = rho < a.rows && ii >= a.w - we;
-  const int rpos = L - a.w + ii;
-  const double2 nz = rval ? a.rowz[(size_t)bg * a.rows_pad + rho] : make_double2(0.0, 0.0);
-  const bool live = rval && nz.y > 0.0;
-  const size_t qoff = (((size_t)b * a.Hq + (size_t)g * a.G) * a.w + (rho < a.rows ? rho : 0)) * a.D;
-  const size_t krow0 = ((size_t)b * a.Hkv + g) * (size_t)a.max_len;
-  for (int m = bid_x(); m < nb; m += a.band_wgs) {
-    const int j = a.band_idx[(size_t)bg * kBandCap + m];
-    const int t0 = max(j - half, c0), t1 = min(j + half, c1 - 1);
-    double pooled = a.pool == SNAP_POOL_MAX ? -1.0 : 0.0;
-    for (int t = t0; t <= t1; ++t) {
-      double wgt = 0.0;
-      if (live && t <= rpos) {
-        double dot = 0.0;
-        if (a.in_f32) {
-          const float* qr = (const float*)a.q + qoff;
-          const float* kr = (const float*)a.k + (krow0 + t) * a.D;
-          for (int d = 0; d < a.D; ++d) dot = fma((double)qr[d], (double)kr[d], dot);
-        } else {
-          const uint16_t* qr = (const uint16_t*)a.q + qoff;
-          const uint16_t* kr = (const uint16_t*)a.k + (krow0 + t) * a.D;
-          for (int d = 0; d < a.D; d += 8) {
-            const u32x4 qv = *(const u32x4*)(qr + d), kv = *(const u32x4*)(kr + d);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              dot = fma((double)bf16_bits_to_f32(qv[e] & 0xffffu), (double)bf16_bits_to_f32(kv[e] & 0xffffu), dot);
-              dot = fma((double)bf16_bits_to_f32(qv[e] >> 16), (double)bf16_bits_to_f32(kv[e] >> 16), dot);
-            }
-          }
-        }
-        wgt = exp2(dot * a.scale2 - nz.x) / nz.y;
-      }
-      const double At = block_sum_f64(wgt, lds);
-      if (a.pool == SNAP_POOL_MAX)
-        pooled = At > pooled ? At : pooled;
-      else
-        pooled += At;
-    }
-    if (tid() == 0) {
-      if (a.pool != SNAP_POOL_MAX) pooled /= (double)a.pool_kernel;
-      a.band_p[(size_t)bg * kBandCap + m] = pooled;
-      if (a.pooled_out) a.pooled_out[(size_t)bg * a.max_len + j] = (float)pooled;
-    }
+  const int c0 = a.sink, c1 = L - a.recent, half = a.pool_kernel / 2;
+  for (int i = tid(); i < nb; i += nthreads()) mem[i] = a.band_idx[(size_t)bg * kBandCap + i];
+  __syncthreads();
+  const int nkeys = band_keys(mem, nb, half, c0, c1, tok, first, scan_lds);
+  if (nkeys > kBandKeyCap) return;
+  // threads per score row (rows_pad <= 256, or 128 for fp32 inputs)
+  if (a.in_f32) {
+    if (a.D == 64) band_rescore_body<float, 64, 8>(a, bg, b, g, nkeys, tok, first, nb, half, c0, L, kl, red);
+    else band_rescore_body<float, 128, 8>(a, bg, b, g, nkeys, tok, first, nb, half, c0, L, kl, red);
+  } else {
+    if (a.D == 64) band_rescore_body<uint16_t, 64, 4>(a, bg, b, g, nkeys, tok, first, nb, half, c0, L, kl, red);
+    else if (a.D == 128) band_rescore_body<uint16_t, 128, 4>(a, bg, b, g, nkeys, tok, first, nb, half, c0, L, kl, red);
+    else band_rescore_body<uint16_t, 576, 8>(a, bg, b, g, nkeys, tok, first, nb, half, c0, L, kl, red);
   }
 }
 
-// One workgroup per group: rank the band members by (fp64 pooled score
-// descending, token index ascending), keep as many as the K_eff - (members
-// above the band) places left, and rewrite the members' P so that the
-// ordered compaction keeps exactly the candidates above the band and the kept
-// members: P > hi for kept ones, 0 for the others, threshold hi, no ties.
+// One workgroup per group: pool each member from the fp64 A of its window
+// (Eq. 2), rank the members by (fp64 pooled score descending, token index
+// ascending), keep the first K_eff - (candidates above the band), and
+// rewrite the members' P so that the ordered compaction keeps exactly the
+// candidates above the band and the kept members: P > hi for kept ones, 0
+// for the others, threshold hi, no ties.
 __global__ __launch_bounds__(kSelThreads) void band_decide(BandArgs a) {
   __shared__ double sp[kBandCap];
   __shared__ int32_t sj[kBandCap];
+  __shared__ int32_t tok[kBandCap];
+  __shared__ int32_t first[kBandCap + 1];
   __shared__ uint32_t lds[8];
   const int bg = bid_x();
   RadixState st = load_state(&a.state[bg]);
   if (st.mode != 2) return;
   const int nb = uniform(a.band_n[bg]);
   if (nb > kBandCap) return;
+  const int b = bg / a.Hkv;
+  int L = uniform(a.lengths[b]);
+  L = L < 0 ? 0 : (L > a.max_len ? a.max_len : L);
+  const int c0 = a.sink, c1 = L - a.recent, half = a.pool_kernel / 2;
+  for (int i = tid(); i < nb; i += nthreads()) sj[i] = a.band_idx[(size_t)bg * kBandCap + i];
+  __syncthreads();
+  if (band_keys(sj, nb, half, c0, c1, tok, first, lds) > kBandKeyCap) return;  // as band_rescore
   uint32_t lo, hi;
   band_limits(st.prefix, lo, hi);
-  // members above the band (all kept)
+  // candidates above the band (all kept)
   uint32_t above = 0;
   for (int s = tid(); s < a.n_splits; s += nthreads()) above += a.band_above[(size_t)bg * a.n_splits + s];
   uint32_t n_above;
   block_exclusive_scan(above, lds, n_above);
   const int need = st.keff - (int)n_above;  // in [1, nb] (tau itself is a member)
   if (need < 0 || need > nb) return;         // not for finite scores; the fp32 selection stands
-  for (int i = tid(); i < kBandCap; i += nthreads()) {
-    sp[i] = i < nb ? a.band_p[(size_t)bg * kBandCap + i] : -2.0;   // pads sort last
-    sj[i] = i < nb ? a.band_idx[(size_t)bg * kBandCap + i] : 0x7fffffff;
+  const double* Ag = a.A64 + (size_t)bg * kBandKeyCap * kBandMaxPass;
+  const int npass = (a.rows_pad + a.rows_per_pass - 1) / a.rows_per_pass;
+  for (int i = tid(); i < nb; i += nthreads()) {
+    const int j = sj[i];
+    const int t0 = max(j - half, c0), t1 = min(j + half, c1 - 1);
+    double pooled = a.pool == SNAP_POOL_MAX ? -1.0 : 0.0;
+    for (int t = t0; t <= t1; ++t) {
+      // key index of t: the first member (by token) whose window holds t
+      // owns it (see band_keys)
+      int lo = 0, hi2 = nb - 1;
+      while (lo < hi2) {
+        const int mid = (lo + hi2) >> 1;
+        if (tok[mid] >= t - half) hi2 = mid; else lo = mid + 1;
+      }
+      int k0 = max(tok[lo] - half, c0);
+      if (lo > 0) k0 = max(k0, tok[lo - 1] + half + 1);
+      const int x = first[lo] + (t - k0);
+      double At = 0.0;
+      for (int pp = 0; pp < npass; ++pp) At += Ag[(size_t)x * kBandMaxPass + pp];
+      if (a.pool == SNAP_POOL_MAX)
+        pooled = At > pooled ? At : pooled;
+      else
+        pooled += At;
+    }
+    if (a.pool != SNAP_POOL_MAX) pooled /= (double)a.pool_kernel;
+    sp[i] = pooled;
+    a.band_p[(size_t)bg * kBandCap + i] = pooled;
+    if (a.pooled_out) a.pooled_out[(size_t)bg * a.max_len + j] = (float)pooled;
   }
   __syncthreads();
-  // bitonic sort of kBandCap entries, first = (score desc, index asc)
-  for (int size = 2; size <= kBandCap; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid(); i < kBandCap; i += nthreads()) {
-        const int jx = i ^ stride;
-        if (jx > i) {
-          const bool asc = (i & size) == 0;  // this pair sorts "first before second"
-          const double pi = sp[i], pj = sp[jx];
-          const int ji = sj[i], jj = sj[jx];
-          const bool i_first = pi > pj || (pi == pj && ji < jj);
-          if (asc != i_first) {
-            sp[i] = pj; sp[jx] = pi;
-            sj[i] = jj; sj[jx] = ji;
-          }
-        }
-      }
-      __syncthreads();
-    }
+  // rank by (score desc, token asc): kept when fewer than `need` come first
+  float* Pg = a.P + (size_t)bg * a.max_len;
+  for (int i = tid(); i < nb; i += nthreads()) {
+    const double pi = sp[i];
+    const int ji = sj[i];
+    int r = 0;
+    for (int u = 0; u < nb; ++u) r += sp[u] > pi || (sp[u] == pi && sj[u] < ji);
+    tok[i] = r < need;
   }
+  __syncthreads();
   // per-split counts of what the compaction keeps: the candidates above the
   // band and the kept members
-  const int c0 = a.sink;
   for (int s = tid(); s < a.n_splits; s += nthreads()) {
     uint32_t n = a.band_above[(size_t)bg * a.n_splits + s];
-    for (int i = 0; i < need; ++i) n += (sj[i] - c0) / kCandChunk == s;
+    for (int i = 0; i < nb; ++i) n += tok[i] && (sj[i] - c0) / kCandChunk == s;
     a.counts[(size_t)bg * a.n_splits + s] = make_uint2(n, 0u);
   }
-  float* Pg = a.P + (size_t)bg * a.max_len;
-  for (int i = tid(); i < nb; i += nthreads()) Pg[sj[i]] = __uint_as_float(i < need ? hi + 1u : 0u);
+  for (int i = tid(); i < nb; i += nthreads()) Pg[sj[i]] = __uint_as_float(tok[i] ? hi + 1u : 0u);
   if (tid() == 0) {
     st.prefix = hi;
     st.krem = 0;
@@ -1298,6 +1432,8 @@ Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   off = align256(off + (size_t)groups * kBandCap * sizeof(double));
   g.off_band_above = off;
   off = align256(off + (size_t)groups * g.n_splits * sizeof(uint32_t));
+  g.off_A64 = off;
+  off = align256(off + (size_t)groups * kBandKeyCap * kBandMaxPass * sizeof(double));
   g.compress_bytes = off;
   return g;
 }
@@ -1358,6 +1494,7 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   int32_t* band_idx = (int32_t*)(w + geo.off_band_idx);
   double* band_p = (double*)(w + geo.off_band_p);
   uint32_t* band_above = (uint32_t*)(w + geo.off_band_above);
+  double* A64 = (double*)(w + geo.off_A64);
 
   ScoreArgs sa;
   sa.q = q_obs;
@@ -1460,6 +1597,7 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
     ba.state = state;
     ba.band_n = band_n;
     ba.band_idx = band_idx;
+    ba.A64 = A64;
     ba.band_p = band_p;
     ba.pooled_out = pooled_out;
     ba.P = P;
@@ -1481,8 +1619,11 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
     ba.n_splits = geo.n_splits;
     ba.in_f32 = !bf;
     ba.band_wgs = kBandWGs;
+    // query-dim slices per score row: 8 for 576-wide bf16 rows and for fp32
+    // rows, else 4 (as band_rescore dispatches)
+    ba.rows_per_pass = kBandThreads / ((!bf || p.d_qk == 576) ? 8 : 4);
     ba.scale2 = (double)scale * 1.4426950408889634074;
-    hipLaunchKernelGGL(band_rescore, dim3(kBandWGs, groups), dim3(256), 0, stream, ba);
+    hipLaunchKernelGGL(band_rescore, dim3(kBandWGs, groups), dim3(kBandThreads), 0, stream, ba);
     hipLaunchKernelGGL(band_decide, dim3(groups), dim3(kSelThreads), 0, stream, ba);
     hipLaunchKernelGGL(select_write, sgrid, dim3(kSelThreads), 0, stream, se);
     if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;

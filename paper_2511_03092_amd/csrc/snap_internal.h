@@ -107,7 +107,7 @@ struct Geometry {
   int n_rowblocks;   // assemble row blocks per group
   size_t off_stats, off_rowref, off_A, off_P, off_hist, off_state, off_counts, off_sel, off_amax;
   // fp64 re-score of the candidates next to the selection threshold
-  size_t off_rowz, off_band_n, off_band_idx, off_band_p, off_band_above;
+  size_t off_rowz, off_band_n, off_band_idx, off_band_p, off_band_above, off_A64;
   size_t compress_bytes;
   // prefill (compress workspace followed by the window queries and V^T)
   int ld_vt;        // keys per V^T row (max_len rounded up to the key tile)
@@ -123,7 +123,7 @@ constexpr int kKeyTile = 64;      // key chunks of the score passes are multiple
 constexpr int kCandChunk = 2048;  // candidates per pool/select workgroup
 constexpr int kSelThreads = 256;
 constexpr int kRadixBins = 2048;
-// Candidates whose pooled score lies within a factor 1 +- 2^-14 of the K-th
+// Candidates whose pooled score lies within a factor 1 +- 2^-17 of the K-th
 // largest are re-scored in fp64 before the final selection, up to this many
 // per (sequence, KV head); a group with more keeps its fp32 selection.
 constexpr int kBandCap = 512;
