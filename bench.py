@@ -128,6 +128,23 @@ def measured_traffic(workload: str):
     return rec["traffic_bytes_per_launch"]
 
 
+def measured_mfma(workload: str):
+    """MFMA utilisation of the workload's score kernels (or the prefill
+    attention, records keyed "prefill:" + workload) from the committed counter
+    runs (profiles/mfma.json: MfmaUtil = MFMA-busy cycles over active cycles of
+    every SIMD, per kernel), or None when no record exists or the kernels'
+    machine code has changed since the counters were taken."""
+    try:
+        rec = json.load(open(os.path.join(HERE, "profiles", "mfma.json")))[workload]
+    except (OSError, KeyError, ValueError):
+        return None
+    code = device_code_sha256(os.path.join(HERE, "paper_2511_03092_amd", "libsnapstream.so"), rec["kernels"])
+    if code is None or code != rec.get("device_code_sha256"):
+        return None
+    return {"mfma_util": rec["mfma_util"], "mfma_bf16_flops_per_launch": rec["mfma_bf16_flops_per_launch"],
+            "source": "rocprofv3 counters, profiles/mfma.json"}
+
+
 def copy_calibration(torch, nbytes, dev):
     """One device-to-device copy of nbytes: the reference that scales the HBM
     byte counters (FETCH_SIZE / WRITE_SIZE) of a counter run."""
@@ -355,7 +372,8 @@ def main():
         "compress_ms_per_seq_layer": round(comp_ms / n, 4),
         "score_gemm": {"gflop_per_layer_call_one_pass": round(score_flop / 1e9, 2), "passes": 2,
                        "tflops_over_compress_call": round(score_tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
-                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4)},
+                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4),
+                       "counters": measured_mfma(wl.name)},
         "roofline": {"bound": "hbm",
                      "kernel": ("snap_cache_append + snap_decode_attn" if args.two_calls else
                                 "snap_decode_step (append + split-K attention, one launch) + combine"),
@@ -557,7 +575,8 @@ def run_cb(args, wl):
         "compress_ms_per_seq_layer": round(comp_ms, 4),
         "score_gemm": {"gflop_per_layer_call_one_pass": round(score_flop / 1e9, 2), "passes": 2,
                        "tflops_over_compress_call": round(score_tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
-                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4)},
+                       "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4),
+                       "counters": measured_mfma(wl.name)},
         "roofline": {"bound": "hbm",
                      "kernel": "snap_decode_step (fp8 cache: append + split-K attention, one launch) + combine"
                                + (", fp8 Q K^T" if args.fp8_qk else ""),
@@ -705,7 +724,8 @@ def run_prefill(args, wl):
                      "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic("prefill:" + wl.name),
-                     "algorithmic_flops_per_launch": flop},
+                     "algorithmic_flops_per_launch": flop,
+                     "mfma_counters": measured_mfma("prefill:" + wl.name)},
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:
@@ -725,6 +745,19 @@ def cpu_model():
     return None
 
 
+def cpu_threads():
+    """Threads for the oracle baseline: the CPUs this process may run on, at
+    most 16 (a GPU's CPU share on the machines this runs on), and the counts
+    behind that choice for the report."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count() or 1
+    T = max(1, min(avail, 16))
+    return T, {"host_logical_cpus": os.cpu_count(), "affinity_cpus": avail, "threads_used": T,
+               "thread_cap": "16: one GPU's CPU share"}
+
+
 def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
     """The fp64 oracle's causal attention on the host's cores, on a bounded
     sample: the last rows of one query head at the longest prompt (each row
@@ -740,7 +773,7 @@ def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
     import oracle
     import synth
 
-    T = max(1, min(os.cpu_count() or 1, 16))
+    T, cpus = cpu_threads()
     op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
                        p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
     L = max(lengths)
@@ -774,7 +807,7 @@ def cpu_baseline_prefill(wl, p, lengths, layers, gpu_value, budget_s=10.0):
     val1 = tokens / (total_macs / rate1)
     valT = tokens / (total_macs / rateT)
     return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
-            "cpu_model": cpu_model(), "single_thread_value": float(f"{val1:.6g}"),
+            "cpu_model": cpu_model(), "cpus": cpus, "single_thread_value": float(f"{val1:.6g}"),
             "sample": (f"causal attention rows {L - nrow}..{L - 1} of one head at L={L} (fp64 oracle): "
                        f"{t1:.2f} s on one thread, the same rows of {T} heads on {T} threads in {tT:.2f} s; "
                        f"extrapolated by multiply-adds to every head and position of {len(lengths)} prompt(s), "
@@ -799,7 +832,7 @@ def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_valu
     import oracle
     import synth
 
-    T = max(1, min(os.cpu_count() or 1, 16))
+    T, cpus = cpu_threads()
     op = oracle.Params(p.n_q_heads, p.n_kv_heads, p.d_qk, p.d_v, p.sink, p.recent, p.topk, p.obs_window,
                        p.pool_kernel, p.pool, p.norm, bool(p.v_in_k), p.sm_scale)
     L = max(comp_lengths)
@@ -842,7 +875,7 @@ def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_valu
     val1 = tokens / (t_comp1 * scale + t_dec1 * units_dec)
     valT = tokens / (t_compT * scale + t_decT * units_dec)
     return {"value": float(f"{valT:.6g}"), "unit": "tok/s", "cores": T, "kind": "oracle",
-            "cpu_model": cpu_model(), "single_thread_value": float(f"{val1:.6g}"),
+            "cpu_model": cpu_model(), "cpus": cpus, "single_thread_value": float(f"{val1:.6g}"),
             "sample": (f"compress units (1 sequence x 1 KV head, L={L}): 1 alone at {t_comp1:.2f} s, then {T} "
                        f"on {T} threads at {t_compT:.2f} s each; decode units (1 sequence x 1 KV head x 1 "
                        f"step): {n_dec} alone at {t_dec1 * 1e3:.1f} ms, then {T * per} on {T} threads at "
