@@ -272,7 +272,9 @@ snap_status snap_decode_step_noalloc(const snap_params* p, const snap_cache* cac
                                      const void* k_new, const void* v_new, void* out, int32_t out_dtype,
                                      void* stream);
 
-/* pos[slot_ids[b]] += 1 for b < n (once per decode step, after every layer).
+/* The decode position moves on by one token (Sec. III-C: each generated token
+ * takes the next position, and the ring row follows from it):
+ * pos[slot_ids[b]] += 1 for b < n (once per decode step, after every layer).
  * pos is device int32[n_slots]; slot ids outside [0, n_slots) are skipped. */
 snap_status snap_advance(int32_t* pos, int32_t n_slots, int32_t n, const int32_t* slot_ids,
                          void* stream);

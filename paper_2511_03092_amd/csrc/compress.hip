@@ -1162,8 +1162,10 @@ __device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff
 // theorem: correctly rounded when neither r nor the quotient leaves the
 // normal range).  Where q0 is 0 or not finite it is kept: the E4M3 code of a
 // zero, of a quotient too small for a non-zero code, or of a saturated one
-// does not depend on the correction.  Checked against the division on every
-// finite bf16 x over several thousand scales: identical E4M3 codes.
+// does not depend on the correction.  Checked on the host against the
+// division for every finite bf16 x over 353 scales (amax / 448 of 256 bf16
+// maxima, 64 random magnitudes, powers of two and their neighbours):
+// identical E4M3 codes.
 __device__ __forceinline__ float div_by_scale(float x, float scale, float inv) {
   const float q0 = x * inv;
   const float r = __builtin_fmaf(-q0, scale, x);

@@ -54,12 +54,13 @@ def test_corrected_quotient_gives_the_division_codes():
     rng = np.random.default_rng(11)
     # scales: amax / 448 for random bf16 maxima (the data-driven scales),
     # random magnitudes, and powers of two with their neighbours
-    amax = (rng.integers(0x3400, 0x4c00, 24, dtype=np.uint32) << 16).view(np.float32)
+    amax = (rng.integers(0x3400, 0x4c00, 256, dtype=np.uint32) << 16).view(np.float32)
     scales = list((amax / np.float32(448)).astype(np.float32))
-    scales += list((2.0 ** rng.uniform(-16, 16, 12)).astype(np.float32))
-    for e in (-12, -3, 0, 5):
+    scales += list((2.0 ** rng.uniform(-16, 16, 64)).astype(np.float32))
+    for e in range(-20, 21, 4):
         p = np.float32(2.0 ** e)
         scales += [p, np.nextafter(p, np.float32(0)), np.nextafter(p, np.float32(np.inf))]
+    assert len(scales) == 353
     for b in scales:
         q = _corrected_quotient(xb, np.float32(b))
         got = oracle.quantize(q.astype(np.float64), 1.0)  # codes of the fp32 value q itself
