@@ -279,6 +279,20 @@ snap_status snap_decode_step_noalloc(const snap_params* p, const snap_cache* cac
 snap_status snap_advance(int32_t* pos, int32_t n_slots, int32_t n, const int32_t* slot_ids,
                          void* stream);
 
+/* Device-side checks of the debug build (libsnapstream_debug.so, built with
+ * SNAP_DEBUG_CHECKS): its kernels test the invariants their indexing rests on
+ * (keys inside the prompt, kept tokens inside the candidates, rows inside the
+ * cache budget, chunk counts within the combine's capacity) and, where one
+ * fails, skip the access and record it instead of faulting.  This call waits
+ * for the device (hipDeviceSynchronize), stores the recorded bits in *flags (0
+ * when none failed) and clears them when reset != 0.  A release build stores
+ * 0 and returns SNAP_ERR_UNSUPPORTED.  Bits: 1 score chunk outside the keys,
+ * 2 selection past K_eff, 4 kept token outside the candidates, 8 re-scored key
+ * outside the candidates, 16 decode rows past the budget, 32 new token's row
+ * outside the sink/ring rows, 64 too many split-K chunks, 128 appended row
+ * outside the sink/ring rows, 256 prefill block outside the prompt. */
+snap_status snap_debug_checks(uint32_t* flags, int32_t reset);
+
 /* Static description of a status code. */
 const char* snap_status_str(snap_status s);
 

@@ -7,7 +7,7 @@ first call raises -- there is no other implementation behind these names.
 
 Functions keep the C names (include/snapstream.h):
     snap_compress, snap_prefill, snap_prefill_attn, snap_cache_append, snap_decode_attn, snap_decode_step,
-    snap_decode_step_noalloc, snap_advance,
+    snap_decode_step_noalloc, snap_advance, snap_debug_checks,
     snap_compress_workspace, snap_prefill_workspace, snap_decode_workspace, snap_status_str
 """
 from __future__ import annotations
@@ -18,6 +18,8 @@ from dataclasses import dataclass
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsnapstream.so")
+# the same library built with the device-side invariant checks (build.py --debug)
+DEBUG_LIB_PATH = os.path.join(_HERE, "libsnapstream_debug.so")
 
 SNAP_OK, SNAP_ERR_INVALID_ARG, SNAP_ERR_UNSUPPORTED, SNAP_ERR_WORKSPACE, SNAP_ERR_HIP = range(5)
 SNAP_F32, SNAP_BF16, SNAP_FP8_E4M3 = 0, 1, 2
@@ -27,8 +29,8 @@ SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
 
 EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_prefill_workspace", "snap_compress",
             "snap_prefill", "snap_prefill_attn", "snap_cache_append",
-            "snap_decode_attn", "snap_decode_step", "snap_decode_step_noalloc", "snap_advance", "snap_status_str",
-            "snap_last_error"]
+            "snap_decode_attn", "snap_decode_step", "snap_decode_step_noalloc", "snap_advance", "snap_debug_checks",
+            "snap_status_str", "snap_last_error"]
 
 
 class SnapParams(ctypes.Structure):
@@ -56,12 +58,26 @@ _lib = None
 def lib() -> ctypes.CDLL:
     """The loaded HIP library; raises if it has not been built."""
     global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2511_03092_amd.build` "
+    if _lib is None:
+        _lib = load(LIB_PATH)
+    return _lib
+
+
+def use_library(path: str) -> ctypes.CDLL:
+    """Route every call of this module to the library at `path` (the release
+    or the debug build); returns the library that was in use."""
+    global _lib
+    prev = lib()
+    _lib = load(path)
+    return prev
+
+
+def load(path: str) -> ctypes.CDLL:
+    """Load one build of the library and declare its entry points."""
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2511_03092_amd.build` "
                           "(there is no fallback implementation)")
-    L = ctypes.CDLL(LIB_PATH)
+    L = ctypes.CDLL(path)
     P, vp, i32, sz = ctypes.POINTER(SnapParams), ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     C = ctypes.POINTER(SnapCache)
     L.snap_compress_workspace.argtypes = [P, i32, i32]
@@ -90,7 +106,8 @@ def lib() -> ctypes.CDLL:
     L.snap_status_str.restype = ctypes.c_char_p
     L.snap_last_error.argtypes = []
     L.snap_last_error.restype = ctypes.c_char_p
-    _lib = L
+    L.snap_debug_checks.argtypes = [ctypes.POINTER(ctypes.c_uint32), i32]
+    L.snap_debug_checks.restype = ctypes.c_int
     return L
 
 
@@ -223,6 +240,14 @@ def snap_decode_step_noalloc(p: Params, cache: SnapCache, pos, n_topk, slot_ids,
 def snap_advance(pos, slot_ids, stream=None):
     _check(lib().snap_advance(_ptr(pos), int(pos.shape[0]), int(slot_ids.shape[0]), _ptr(slot_ids),
                               _stream(stream)))
+
+
+def snap_debug_checks(reset: bool = True) -> int:
+    """The invariant bits the debug build's kernels recorded (waits for the
+    device); raises SnapError on a release build."""
+    flags = ctypes.c_uint32(0)
+    _check(lib().snap_debug_checks(ctypes.byref(flags), int(reset)))
+    return int(flags.value)
 
 
 def workspace(nbytes: int, device="cuda"):

@@ -313,6 +313,24 @@ snap_status snap_decode_step_noalloc(const snap_params* p, const snap_cache* cac
   return st;
 }
 
+snap_status snap_debug_checks(uint32_t* flags, int32_t reset) {
+  g_err[0] = 0;
+  if (!flags) return fail(SNAP_ERR_INVALID_ARG, "flags is NULL");
+  *flags = 0;
+#ifdef SNAP_DEBUG_CHECKS
+  if (hipDeviceSynchronize() != hipSuccess) return fail(SNAP_ERR_HIP, "hipDeviceSynchronize failed");
+  const uint32_t c = debug_flags_compress(reset != 0), d = debug_flags_decode(reset != 0),
+                 f = debug_flags_prefill(reset != 0);
+  if (c == 0xffffffffu || d == 0xffffffffu || f == 0xffffffffu)
+    return fail(SNAP_ERR_HIP, "reading the check words failed");
+  *flags = c | d | f;
+  return SNAP_OK;
+#else
+  (void)reset;
+  return fail(SNAP_ERR_UNSUPPORTED, "a release build: no device-side checks (build with --debug)");
+#endif
+}
+
 snap_status snap_advance(int32_t* pos, int32_t n_slots, int32_t n, const int32_t* slot_ids, void* stream) {
   g_err[0] = 0;
   if (n < 0 || n_slots < 1) return fail(SNAP_ERR_INVALID_ARG, "need n >= 0 and n_slots >= 1");

@@ -270,7 +270,8 @@ __global__ __launch_bounds__(NW * 64) void score_pass(ScoreArgs a) {
     hi = L;
   }
   const int c0 = lo + bid_x() * a.key_chunk;
-  const int c1 = min(c0 + a.key_chunk, hi);
+  int c1 = min(c0 + a.key_chunk, hi);
+  if (!debug_check(c0 >= 0 && c1 <= a.max_len, kDbgScoreRange)) c1 = c0;  // skip the chunk
   const int we = min(a.w, L);
   const bool wave_has_rows = wave * 32 < a.rows;
 
@@ -871,7 +872,8 @@ __device__ void band_rescore_body(const BandArgs& a, int bg, int b, int g, int n
     for (int i = tid(); i < nk * kRowChunks; i += nthreads()) {
       const int e = i / kRowChunks, c = i % kRowChunks;
       const int t = band_key_token(tok, first, nb, half, c0, x0 + e);
-      *((u32x4*)kl + i) = *((const u32x4*)((const In*)a.k + (krow0 + t) * D) + c);
+      if (debug_check(t >= c0 && t < L - a.recent, kDbgBand))
+        *((u32x4*)kl + i) = *((const u32x4*)((const In*)a.k + (krow0 + t) * D) + c);
     }
     int kt[kBandKeys];
 #pragma unroll
@@ -1105,7 +1107,7 @@ __global__ __launch_bounds__(kSelThreads) void select_write(SelectArgs a) {
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i)
     if (keep[i]) {
-      if (pos < keff) sg[pos] = jt + i;  // never past the group's K slots
+      if (debug_check(pos < keff, kDbgSelWrite) && pos < keff) sg[pos] = jt + i;  // never past the group's K slots
       ++pos;
     }
 }
@@ -1153,7 +1155,9 @@ __device__ __forceinline__ int row_source(int row, int L, int s, int r, int keff
     return t < L ? t : -1;
   }
   int m = row - s - r;
-  return m < keff ? sel[m] : -1;
+  if (m >= keff) return -1;
+  const int t = sel[m];
+  return debug_check(t >= s && t < L - r, kDbgAsmSource) ? t : -1;
 }
 
 // x / scale rounded once to fp32, as an IEEE division gives it, from a
@@ -1377,6 +1381,8 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
 
 // ============================================================ host side
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+SNAP_DEBUG_READER(debug_flags_compress)
 
 Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
   Geometry g{};

@@ -76,7 +76,7 @@ __device__ __forceinline__ bool span_of(const DecodeArgs& a, int b, int chunk, i
   sp.nv = nv;
   sp.v0 = chunk * cs;
   sp.v1 = min(sp.v0 + cs, nv);
-  return true;
+  return debug_check(nv <= sr + a.topk, kDbgDecodeSpan);
 }
 
 // ---------------------------------------------------------------- fp8 -> bf16
@@ -164,7 +164,8 @@ __device__ __forceinline__ int new_row(const DecodeArgs& a, int slot) {
   if (!a.k_new) return -1;
   const int p = __builtin_amdgcn_readfirstlane(a.pos[slot]);
   if (p < 0) return -1;
-  return p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
+  const int row = p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
+  return debug_check(row < a.sink + a.recent, kDbgDecodeNew) ? row : -1;
 }
 
 // Chunk 0 of (slot, KV head g) stores the new k (and v) row, one 16-byte
@@ -974,6 +975,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   const int bh = bid_x(), b = bh / a.Hq;
   const int slot = a.slot_ids[b];
   if (slot < 0 || slot >= a.n_slots) return;
+  if (!debug_check(a.n_chunks <= kMaxChunks, kDbgCombine)) return;
   const int lane = tid() & 63, wave = tid() >> 6;
   const int d = bid_y() * kCombineThreads + tid();
   const float* part = a.part + (size_t)bh * a.n_chunks * a.dv + d;
@@ -1085,6 +1087,7 @@ __global__ __launch_bounds__(256) void append(AppendArgs a) {
   if (p < 0) return;
   const int s = a.sink, r = a.recent, B = s + r + a.topk;
   const int row = p < s ? p : s + (p - s) % r;
+  if (!debug_check(row < s + r, kDbgAppend)) return;
   const int kc = a.dk / 8, vc = a.v_new ? a.dv / 8 : 0;
   for (int i = tid(); i < a.Hkv * (kc + vc); i += nthreads()) {
     const int g = i / (kc + vc), c = i % (kc + vc);
@@ -1111,6 +1114,8 @@ __global__ __launch_bounds__(256) void advance(int32_t* pos, int n_slots, int n,
 
 // ---------------------------------------------------------------- host side
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+SNAP_DEBUG_READER(debug_flags_decode)
 
 // workgroups per call for the LDS-staged latent decode: one per CU, all
 // resident at once (more, smaller chunks measured slower: each workgroup pays

@@ -146,6 +146,7 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
   const int P = a.P;
   const int top = L - P * kblk;  // one past this workgroup's last position
   if (top <= 0) return;
+  if (!debug_check(top <= L && L <= a.max_len, kDbgPrefill)) return;
   const int pos0 = top - P;  // first position (negative in a partial block)
   const int nt = (top + kPfTK - 1) / kPfTK;
   const float s2 = a.scale2;
@@ -377,6 +378,8 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
 
 // ============================================================ host side
 static inline size_t align256p(size_t x) { return (x + 255) & ~(size_t)255; }
+
+SNAP_DEBUG_READER(debug_flags_prefill)
 
 Geometry prefill_geometry(const snap_params& p, int n_seq, int max_len) {
   Geometry g = compress_geometry(p, n_seq, max_len);

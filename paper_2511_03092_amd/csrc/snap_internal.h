@@ -96,6 +96,51 @@ __device__ __forceinline__ float warp_sum(float v) {
   return v;
 }
 
+// ---------------------------------------------------------------- debug checks
+// Built with SNAP_DEBUG_CHECKS (libsnapstream_debug.so), kernels test the
+// invariants their indexing rests on and record a violated one as a bit of a
+// device word (one per source file), skipping the access the check guards,
+// instead of faulting; snap_debug_checks() reads the words.  Release builds
+// compile the checks away.
+enum : uint32_t {
+  kDbgScoreRange = 1u << 0,  // a score chunk's keys outside [0, max_len)
+  kDbgSelWrite = 1u << 1,    // the ordered compaction would write past K_eff
+  kDbgAsmSource = 1u << 2,   // a kept row's token outside the candidates
+  kDbgBand = 1u << 3,        // a re-scored key outside the candidates
+  kDbgDecodeSpan = 1u << 4,  // decode rows past sink + recent + topk
+  kDbgDecodeNew = 1u << 5,   // the new token's row outside the sink / ring rows
+  kDbgCombine = 1u << 6,     // more split-K chunks than the combine holds
+  kDbgAppend = 1u << 7,      // an appended row outside the sink / ring rows
+  kDbgPrefill = 1u << 8,     // a prefill block's positions outside the prompt
+};
+#ifdef SNAP_DEBUG_CHECKS
+static __device__ uint32_t g_debug_flags;  // one per translation unit
+__device__ __forceinline__ bool debug_check(bool ok, uint32_t bit) {
+  if (!ok) atomicOr(&g_debug_flags, bit);
+  return ok;
+}
+// host side: this file's word (and clear it)
+#define SNAP_DEBUG_READER(name)                                                     \
+  uint32_t name(bool reset) {                                                      \
+    uint32_t v = 0;                                                                \
+    if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_debug_flags), sizeof(v)) != hipSuccess) \
+      return 0xffffffffu;                                                          \
+    if (reset) {                                                                   \
+      const uint32_t z = 0;                                                        \
+      if (hipMemcpyToSymbol(HIP_SYMBOL(g_debug_flags), &z, sizeof(z)) != hipSuccess) \
+        return 0xffffffffu;                                                        \
+    }                                                                              \
+    return v;                                                                      \
+  }
+#else
+__device__ __forceinline__ bool debug_check(bool, uint32_t) { return true; }
+#define SNAP_DEBUG_READER(name) \
+  uint32_t name(bool) { return 0; }
+#endif
+uint32_t debug_flags_compress(bool reset);
+uint32_t debug_flags_decode(bool reset);
+uint32_t debug_flags_prefill(bool reset);
+
 // ---------------------------------------------------------------- launch context
 struct Geometry {
   // compress

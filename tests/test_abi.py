@@ -37,6 +37,19 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n), n
 
 
+def test_debug_build_exports_the_same_symbols_and_release_refuses_checks():
+    """The debug build (device-side invariant checks) has the same entry
+    points; the release build answers snap_debug_checks with
+    SNAP_ERR_UNSUPPORTED and zero flags, without touching the device."""
+    D = snap.load(snap.DEBUG_LIB_PATH)
+    for n in _declared():
+        assert hasattr(D, n), n
+    flags = ctypes.c_uint32(7)
+    assert snap.lib().snap_debug_checks(ctypes.byref(flags), 1) == snap.SNAP_ERR_UNSUPPORTED
+    assert flags.value == 0
+    assert snap.lib().snap_debug_checks(None, 1) == snap.SNAP_ERR_INVALID_ARG
+
+
 def test_status_strings():
     for s in range(5):
         assert snap.snap_status_str(s)
