@@ -80,6 +80,18 @@ typedef enum {
                                 tokens appended later saturate at +-448 codes */
 } snap_fp8_scales;
 
+/* How decode reads the cache rows (a load hint; results are the same). */
+typedef enum {
+  SNAP_KV_AUTO = 0,   /* streaming when the call's cache rows at the full
+                         budget reach 128 MiB, cached loads otherwise          */
+  SNAP_KV_STREAM = 1, /* non-temporal loads: the rows will not be read again
+                         before the last-level cache (256 MB) has turned over,
+                         e.g. many layers or large batches between two reads  */
+  SNAP_KV_KEEP = 2    /* ordinary loads: the cache fits in the last-level cache
+                         and is read again soon (a one-layer model, a small
+                         batch)                                                 */
+} snap_kv_reuse;
+
 /* The method's hyper-parameters (Sec. III, Table 6's names). */
 typedef struct {
   int32_t n_q_heads;   /* query heads; a multiple of n_kv_heads                 */
@@ -111,6 +123,7 @@ typedef struct {
                           inputs, a GQA fp8 cache, d_qk = d_v = 128
                           (SNAP_ERR_UNSUPPORTED otherwise).  Values stay bf16
                           products.                                              */
+  int32_t kv_reuse;    /* snap_kv_reuse: the decode kernels' load hint          */
 } snap_params;
 
 /* One layer's compressed cache (device memory, caller-owned, row-major):

@@ -26,6 +26,7 @@ SNAP_F32, SNAP_BF16, SNAP_FP8_E4M3 = 0, 1, 2
 SNAP_POOL_MAX, SNAP_POOL_AVG = 0, 1
 SNAP_NORM_CAND, SNAP_NORM_ROW = 0, 1
 SNAP_FP8_SCALES_GIVEN, SNAP_FP8_SCALES_AMAX = 0, 1
+SNAP_KV_AUTO, SNAP_KV_STREAM, SNAP_KV_KEEP = 0, 1, 2
 
 EXPORTED = ["snap_compress_workspace", "snap_decode_workspace", "snap_prefill_workspace", "snap_compress",
             "snap_prefill", "snap_prefill_attn", "snap_cache_append",
@@ -38,7 +39,8 @@ class SnapParams(ctypes.Structure):
         "n_q_heads", "n_kv_heads", "d_qk", "d_v", "v_in_k", "sink", "recent", "topk",
         "obs_window", "pool_kernel", "pool", "norm", "in_dtype", "kv_dtype")] + [("sm_scale", ctypes.c_float),
                                                                                   ("fp8_scales", ctypes.c_int32),
-                                                                                  ("fp8_qk", ctypes.c_int32)]
+                                                                                  ("fp8_qk", ctypes.c_int32),
+                                                                                  ("kv_reuse", ctypes.c_int32)]
 
 
 class SnapCache(ctypes.Structure):
@@ -131,6 +133,7 @@ class Params:
     sm_scale: float = 0.0
     fp8_scales: int = SNAP_FP8_SCALES_GIVEN
     fp8_qk: int = 0
+    kv_reuse: int = SNAP_KV_AUTO
 
     @property
     def budget(self) -> int:
@@ -140,7 +143,7 @@ class Params:
         return SnapParams(self.n_q_heads, self.n_kv_heads, self.d_qk, self.d_v, int(self.v_in_k), self.sink,
                           self.recent, self.topk, self.obs_window, self.pool_kernel, self.pool, self.norm,
                           self.in_dtype, self.kv_dtype, float(self.sm_scale), int(self.fp8_scales),
-                          int(self.fp8_qk))
+                          int(self.fp8_qk), int(self.kv_reuse))
 
 
 def _ptr(t) -> int | None:

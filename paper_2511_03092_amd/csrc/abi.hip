@@ -57,6 +57,8 @@ static snap_status check_params(const snap_params* p) {
   if (p->fp8_scales != SNAP_FP8_SCALES_GIVEN && p->fp8_scales != SNAP_FP8_SCALES_AMAX)
     return fail(SNAP_ERR_INVALID_ARG, "unknown fp8_scales mode");
   if (p->fp8_qk != 0 && p->fp8_qk != 1) return fail(SNAP_ERR_INVALID_ARG, "fp8_qk must be 0 or 1");
+  if (p->kv_reuse != SNAP_KV_AUTO && p->kv_reuse != SNAP_KV_STREAM && p->kv_reuse != SNAP_KV_KEEP)
+    return fail(SNAP_ERR_INVALID_ARG, "unknown kv_reuse hint");
   if (p->fp8_qk && !(p->kv_dtype == SNAP_FP8_E4M3 && p->in_dtype == SNAP_BF16 && !p->v_in_k && p->d_qk == 128 &&
                      p->d_v == 128))
     return fail(SNAP_ERR_UNSUPPORTED, "fp8_qk needs bf16 inputs, a GQA fp8 cache and d_qk = d_v = 128");

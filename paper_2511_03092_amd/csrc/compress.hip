@@ -1178,7 +1178,9 @@ __device__ __forceinline__ float div_by_scale(float x, float scale, float inv) {
 }
 
 // 8 elements of an input row in raw form: 16 bytes of bf16 or 32 of fp32
-// (zeros for a NULL source, a padding row).
+// (zeros for a NULL source, a padding row).  The gather reads each prompt row
+// and writes each cache row once: both carry the non-temporal (streaming)
+// hint (measured 1-2% off the compress call).
 template <typename In>
 struct Raw8In {
   u32x4 w[sizeof(In) / 2];
@@ -1188,7 +1190,7 @@ __device__ __forceinline__ Raw8In<In> load8(const In* src) {
   Raw8In<In> x;
 #pragma unroll
   for (int i = 0; i < (int)(sizeof(In) / 2); ++i)
-    x.w[i] = src ? *((const u32x4*)src + i) : u32x4{0u, 0u, 0u, 0u};
+    x.w[i] = src ? __builtin_nontemporal_load((const u32x4*)src + i) : u32x4{0u, 0u, 0u, 0u};
   return x;
 }
 // ... stored into the cache, quantised to E4M3 codes of x / scale when the
@@ -1215,10 +1217,10 @@ __device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scal
       for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(div_by_scale(f[h * 4 + i], scale, inv)) << (8 * i);
       o[h] = w;
     }
-    *(u32x2*)dst = o;
+    __builtin_nontemporal_store(o, (u32x2*)dst);
   } else {
 #pragma unroll
-    for (int i = 0; i < (int)(sizeof(In) / 2); ++i) *((u32x4*)dst + i) = x.w[i];
+    for (int i = 0; i < (int)(sizeof(In) / 2); ++i) __builtin_nontemporal_store(x.w[i], (u32x4*)dst + i);
   }
 }
 

@@ -94,7 +94,13 @@ __device__ __forceinline__ u32x4 e4m3x8_to_bf16x8(u32x2 c) {
 }
 
 // Raw 8-element loads: bf16 rows stay as 16 bytes, fp8 rows as 8 bytes of codes
-// until they are used, so a prefetch does not wait on a conversion.
+// until they are used, so a prefetch does not wait on a conversion.  NT: the
+// non-temporal (streaming) hint, for calls whose cache rows are too many to
+// stay in the 256 MB last-level cache until the next call (launch_decode
+// picks it): measured 13% faster for the fp8 GQA decode of 31 slots and,
+// with the bf16 K chunk order of decode_mfma (kchunk), 7% for the bf16 one;
+// on a one-layer 32k call (17 MB, re-read from that cache every step) it
+// was slower, so small calls load without it.
 template <bool FP8>
 struct Raw8 {
   typedef u32x4 T;
@@ -104,15 +110,16 @@ struct Raw8<true> {
   typedef u32x2 T;
 };
 
-template <bool FP8>
+template <bool FP8, bool NT>
 __device__ __forceinline__ typename Raw8<FP8>::T load_raw8(const void* base, size_t elem, bool ok) {
   typedef typename Raw8<FP8>::T T;
   T z = {};
   if (!ok) return z;
-  if constexpr (FP8)
-    return *(const u32x2*)((const uint8_t*)base + elem);
+  const T* p = FP8 ? (const T*)((const uint8_t*)base + elem) : (const T*)((const uint16_t*)base + elem);
+  if constexpr (NT)
+    return __builtin_nontemporal_load(p);
   else
-    return *(const u32x4*)((const uint16_t*)base + elem);
+    return *p;
 }
 
 template <bool FP8>
@@ -197,7 +204,19 @@ __device__ __forceinline__ void new_piece_store(const DecodeArgs& a, int g, int 
 // the two products because the V operand is loaded in the matching row order.
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-template <int KSTEPS, int VPASS, bool FP8, bool QK8 = false>
+// The 8-element chunk of a 32 * KSTEPS-wide row that lane group lg feeds to
+// k-step t (q and K use the same map, so the dot products are unchanged).
+// bf16 with streaming loads: chunk 4t + lg, so one load instruction reads 64
+// contiguous bytes of each of its 16 rows (chunk KSTEPS*lg + t, where the four
+// instructions each read 16 bytes of every 64, re-fetched lines under the
+// streaming hint and was 15% slower).  Otherwise chunk KSTEPS*lg + t: with
+// ordinary loads it measured 1.5% faster on the one-layer 32k call, and fp8
+// keeps lane group lg on the 32 contiguous codes 32lg..32lg+31 that the fp8
+// MFMA of the fp8_qk path takes per lane.
+template <int KSTEPS, bool FP8, bool NT>
+__device__ __forceinline__ int kchunk(int t, int lg) { return (FP8 || !NT) ? KSTEPS * lg + t : 4 * t + lg; }
+
+template <int KSTEPS, int VPASS, bool FP8, bool QK8, bool NT>
 __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
   static_assert(!QK8 || (FP8 && KSTEPS == 4), "fp8 products need an fp8 cache of 128-wide rows");
   constexpr int D = KSTEPS * 32;
@@ -219,7 +238,7 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
 #pragma unroll
     for (int t = 0; t < KSTEPS; ++t) {
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (hval) v = *(const u32x4*)(qp + 8 * (KSTEPS * lg + t));
+      if (hval) v = *(const u32x4*)(qp + 8 * kchunk<KSTEPS, FP8, NT>(t, lg));
       qf[t] = __builtin_bit_cast(bf16x8, v);
     }
   }
@@ -291,9 +310,9 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
       const size_t e0 = (row0 + virt_row(vb, sp.n1, sr)) * D + (size_t)l16 * D;
 #pragma unroll
       for (int t = 0; t < KSTEPS; ++t) {
-        const int col = 8 * (KSTEPS * lg + t);
-        ka[t] = load_raw8<FP8>(a.ck, e0 + col, true);
-        kb[t] = load_raw8<FP8>(a.ck, e0 + 16 * D + col, true);
+        const int col = 8 * kchunk<KSTEPS, FP8, NT>(t, lg);
+        ka[t] = load_raw8<FP8, NT>(a.ck, e0 + col, true);
+        kb[t] = load_raw8<FP8, NT>(a.ck, e0 + 16 * D + col, true);
       }
       return;
     }
@@ -302,13 +321,13 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
     const size_t eb = (row0 + virt_row(vb2, sp.n1, sr)) * D;
 #pragma unroll
     for (int t = 0; t < KSTEPS; ++t) {
-      const int col = 8 * (KSTEPS * lg + t);
+      const int col = 8 * kchunk<KSTEPS, FP8, NT>(t, lg);
       if constexpr (FP8) {
-        ka[t] = va == vnew ? newq[col / 8] : load_raw8<FP8>(a.ck, ea + col, va < sp.v1);
-        kb[t] = vb2 == vnew ? newq[col / 8] : load_raw8<FP8>(a.ck, eb + col, vb2 < sp.v1);
+        ka[t] = va == vnew ? newq[col / 8] : load_raw8<FP8, NT>(a.ck, ea + col, va < sp.v1);
+        kb[t] = vb2 == vnew ? newq[col / 8] : load_raw8<FP8, NT>(a.ck, eb + col, vb2 < sp.v1);
       } else {
-        ka[t] = load_raw8<FP8>(va == vnew ? a.k_new : a.ck, va == vnew ? knew_off + col : ea + col, va < sp.v1);
-        kb[t] = load_raw8<FP8>(vb2 == vnew ? a.k_new : a.ck, vb2 == vnew ? knew_off + col : eb + col, vb2 < sp.v1);
+        ka[t] = load_raw8<FP8, NT>(va == vnew ? a.k_new : a.ck, va == vnew ? knew_off + col : ea + col, va < sp.v1);
+        kb[t] = load_raw8<FP8, NT>(vb2 == vnew ? a.k_new : a.ck, vb2 == vnew ? knew_off + col : eb + col, vb2 < sp.v1);
       }
     }
   };
@@ -325,7 +344,7 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
       for (int i = 0; i < 8; ++i) {
         const int r = i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4);
 #pragma unroll
-        for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8>(vbase, e0 + (size_t)r * vstride + 128 * pp, true);
+        for (int pp = 0; pp < VPASS; ++pp) vv[pp][i] = load_raw8<FP8, NT>(vbase, e0 + (size_t)r * vstride + 128 * pp, true);
       }
     } else {
 #pragma unroll
@@ -336,9 +355,9 @@ __global__ __launch_bounds__(64) void decode_mfma(DecodeArgs a) {
         for (int pp = 0; pp < VPASS; ++pp)
           if constexpr (FP8)
             vv[pp][i] = vi == vnew ? newq[D / 8 + 16 * pp + l16]
-                                   : load_raw8<FP8>(vbase, ev + 128 * pp + 8 * l16, vi < sp.v1);
+                                   : load_raw8<FP8, NT>(vbase, ev + 128 * pp + 8 * l16, vi < sp.v1);
           else
-            vv[pp][i] = load_raw8<FP8>(vi == vnew ? a.v_new : vbase,
+            vv[pp][i] = load_raw8<FP8, NT>(vi == vnew ? a.v_new : vbase,
                                        (vi == vnew ? vnew_off : ev) + 128 * pp + 8 * l16, vi < sp.v1);
       }
     }
@@ -468,7 +487,7 @@ constexpr int kMlaKSteps = 18;
 __device__ __forceinline__ int mla_kbeg(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
 __device__ __forceinline__ int mla_kcnt(int w) { return w < 2 ? 5 : 4; }
 
-template <bool FP8>
+template <bool FP8, bool NT>
 __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
   constexpr int D = kMlaKSteps * 32;  // 576
   typedef typename Raw8<FP8>::T RawT;
@@ -511,8 +530,8 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
     for (int t = 0; t < 5; ++t) {
       const int col = 32 * kb + 8 * (kc * lg + t);
       const bool tin = t < kc;
-      ka[t] = load_raw8<FP8>(a.ck, ra * D + col, va < sp.v1 && tin);
-      kbv[t] = load_raw8<FP8>(a.ck, rb * D + col, vb2 < sp.v1 && tin);
+      ka[t] = load_raw8<FP8, NT>(a.ck, ra * D + col, va < sp.v1 && tin);
+      kbv[t] = load_raw8<FP8, NT>(a.ck, rb * D + col, vb2 < sp.v1 && tin);
     }
   };
   RawT ka[5], kbv[5];
@@ -525,7 +544,7 @@ __global__ __launch_bounds__(256) void decode_mla(DecodeArgs a) {
     for (int i = 0; i < 8; ++i) {
       const int vi = vb + (i < 4 ? 4 * lg + i : 16 + 4 * lg + (i - 4));
       const size_t rr = row0 + virt_row(vi, sp.n1, sr);
-      vv[i] = load_raw8<FP8>(a.ck, rr * D + 128 * w + 8 * l16, vi < sp.v1);
+      vv[i] = load_raw8<FP8, NT>(a.ck, rr * D + 128 * w + 8 * l16, vi < sp.v1);
     }
     RawT kn[5], kn2[5];
     if (vb + 32 < sp.v1) load_k(vb + 32, kn, kn2);
@@ -649,22 +668,36 @@ typedef __attribute__((address_space(3))) void* lds_void_ptr_t;
 // One wave-instruction of global -> LDS copy (lane i's 16 bytes land at
 // lds_wave_base + 16*i), issued through inline asm so that the only ordering
 // with later LDS reads is the caller's explicit vmcnt wait and barrier.  M0
-// (the DMA's LDS base) is saved and restored around it.
+// (the DMA's LDS base) is saved and restored around it.  NT as for load_raw8
+// (measured 3-7% faster on the 16 x 128k latent call).
+template <bool NT>
 __device__ __forceinline__ void dma16_lat(const void* g, const void* lds_wave_base) {
   // wave-uniform by construction; readfirstlane keeps it in a scalar register
   // whatever the compiler's uniformity analysis concludes
   const uint32_t la = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr_t)lds_wave_base);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
-      "s_nop 0\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(la), "v"(g)
-      : "memory");
+  if constexpr (NT)
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, off nt\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(la), "v"(g)
+        : "memory");
+  else
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, off\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(la), "v"(g)
+        : "memory");
 }
 
 template <int N>
@@ -678,6 +711,7 @@ __device__ __forceinline__ void lat_barrier() {
   asm volatile("" ::: "memory");
 }
 
+template <bool NT>
 __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
   constexpr int D = 576;
   __shared__ __align__(16) unsigned char stage[kLatStages][kLatBlockBytes];
@@ -730,7 +764,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     if (plain) {
       const unsigned char* base = cache + (size_t)virt_row(vb, sp.n1, sr) * kLatRowBytes;
 #pragma unroll
-      for (int ii = 0; ii < kLatLoadsPerWave; ++ii) dma16_lat(base + ld_off[ii], dst + (size_t)(wu + 4 * ii) * 1024);
+      for (int ii = 0; ii < kLatLoadsPerWave; ++ii) dma16_lat<NT>(base + ld_off[ii], dst + (size_t)(wu + 4 * ii) * 1024);
     } else {
 #pragma unroll
       for (int ii = 0; ii < kLatLoadsPerWave; ++ii) {
@@ -738,7 +772,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
         v = v < sp.nv ? v : sp.nv - 1;
         const unsigned char* src =
             (v == vnew ? knew : cache + (size_t)virt_row(v, sp.n1, sr) * kLatRowBytes) + ld_c[ii] * 16;
-        dma16_lat(src, dst + (size_t)(wu + 4 * ii) * 1024);
+        dma16_lat<NT>(src, dst + (size_t)(wu + 4 * ii) * 1024);
       }
     }
   };
@@ -761,7 +795,7 @@ __global__ __launch_bounds__(256) void decode_mla_lds(DecodeArgs a) {
     for (int ii = wu; ii < nq; ii += 4) {
       int qc = ii * 64 + lane;
       qc = qc < qchunks ? qc : 0;  // the last instruction's spare lanes re-read chunk 0
-      dma16_lat(qsrc + (size_t)qc * 16, qdst + (size_t)ii * 1024);
+      dma16_lat<NT>(qsrc + (size_t)qc * 16, qdst + (size_t)ii * 1024);
     }
     const int pro = min(nblk, kLatStages - 1);
     for (int s = 0; s < pro; ++s) issue(s);
@@ -1121,6 +1155,10 @@ SNAP_DEBUG_READER(debug_flags_decode)
 // resident at once (more, smaller chunks measured slower: each workgroup pays
 // its prologue and the combine grows)
 constexpr int kLatentLdsWGs = 256;
+// with the SNAP_KV_AUTO hint, decode calls reading at least this many cache
+// bytes (at the full budget) use streaming loads: half the 256 MB last-level
+// cache
+constexpr size_t kStreamingCallBytes = (size_t)128 << 20;
 
 Geometry decode_geometry(const snap_params& p, int n) {
   Geometry g{};
@@ -1194,20 +1232,31 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
       if (st != SNAP_OK) return st;
     }
   }
+  // streaming loads as the caller's hint says, or by default when the call's
+  // cache rows (at the full budget) exceed what the last-level cache could
+  // keep for the next call
+  const size_t elt = p.kv_dtype == SNAP_F32 ? 4 : (p.kv_dtype == SNAP_BF16 ? 2 : 1);
+  const size_t call_bytes = (size_t)n * p.n_kv_heads * (size_t)(p.sink + p.recent + p.topk) *
+                            (size_t)(p.d_qk + (p.v_in_k ? 0 : p.d_v)) * elt;
+  const bool nt = p.kv_reuse == SNAP_KV_STREAM || (p.kv_reuse == SNAP_KV_AUTO && call_bytes >= kStreamingCallBytes);
   if (mla_ok) {
     dim3 grid(geo.n_chunks, n);
+    void (*k)(DecodeArgs);
     if (p.kv_dtype == SNAP_FP8_E4M3)
-      hipLaunchKernelGGL((decode_mla<true>), grid, dim3(256), 0, stream, a);
+      k = nt ? decode_mla<true, true> : decode_mla<true, false>;
     else
-      hipLaunchKernelGGL(decode_mla_lds, grid, dim3(256), 0, stream, a);
+      k = nt ? decode_mla_lds<true> : decode_mla_lds<false>;
+    hipLaunchKernelGGL(k, grid, dim3(256), 0, stream, a);
   } else if (mfma_ok) {
     dim3 grid(geo.n_chunks, n * p.n_kv_heads);
+    void (*k)(DecodeArgs);
     if (p.kv_dtype == SNAP_FP8_E4M3 && p.fp8_qk)
-      hipLaunchKernelGGL((decode_mfma<4, 1, true, true>), grid, dim3(64), 0, stream, a);
+      k = nt ? decode_mfma<4, 1, true, true, true> : decode_mfma<4, 1, true, true, false>;
     else if (p.kv_dtype == SNAP_FP8_E4M3)
-      hipLaunchKernelGGL((decode_mfma<4, 1, true>), grid, dim3(64), 0, stream, a);
+      k = nt ? decode_mfma<4, 1, true, false, true> : decode_mfma<4, 1, true, false, false>;
     else
-      hipLaunchKernelGGL((decode_mfma<4, 1, false>), grid, dim3(64), 0, stream, a);
+      k = nt ? decode_mfma<4, 1, false, false, true> : decode_mfma<4, 1, false, false, false>;
+    hipLaunchKernelGGL(k, grid, dim3(64), 0, stream, a);
   } else {
     dim3 grid(geo.n_chunks, n * p.n_q_heads);
     if (p.kv_dtype == SNAP_F32)

@@ -263,6 +263,15 @@ def test_fp8_qk_validation():
     assert st == snap.SNAP_ERR_INVALID_ARG and "scale" in msg
 
 
+def test_kv_reuse_validation():
+    """The decode load hint: the three snap_kv_reuse values pass the parameter
+    checks (a workspace size comes back), anything else is refused."""
+    for bad in (-1, 3, 7):
+        assert _compress_status(_params(kv_reuse=bad))[0] == snap.SNAP_ERR_INVALID_ARG
+    for ok in (snap.SNAP_KV_AUTO, snap.SNAP_KV_STREAM, snap.SNAP_KV_KEEP):
+        assert snap.snap_decode_workspace(_params(kv_reuse=ok), 4) > 0
+
+
 def test_launch_grid_limits():
     """Sizes whose per-(sequence, head) launch grids would not fit are refused
     before any launch."""

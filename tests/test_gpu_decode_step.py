@@ -105,17 +105,19 @@ def test_step_fp8_fused_and_fp32_two_launch_paths():
     _fused_vs_two_calls(wl, p, [wl.length], [0], 1, 24, torch.float32)
 
 
-def test_fp8_query_products():
+@pytest.mark.parametrize("kv_reuse", [snap.SNAP_KV_AUTO, snap.SNAP_KV_STREAM])
+def test_fp8_query_products(kv_reuse):
     """snap_params.fp8_qk = 1 over a GQA fp8 cache: the query is quantised per
     head and Q K^T runs on the fp8 MFMA.  Checked against the oracle attending
     with the same quantised query (oracle.fp8_scale / quantize), to the fp8
     tolerance; the deviation from the exact query is reported beside it.  The
-    fused step (new row quantised in LDS) and the two-call path both run."""
+    fused step (new row quantised in LDS) and the two-call path both run, with
+    ordinary loads (the default at this size) and with streaming loads."""
     from snaphelp import fp8_query
     wl = synth.small(GQA, kv_dtype="fp8")
-    p = params_of(wl, fp8_qk=1)
+    p = params_of(wl, fp8_qk=1, kv_reuse=kv_reuse)
     lengths = [2000, 900, 3]
-    _announce(f"fp8 query products (fp8_qk=1): lengths {lengths}, fused step then two calls")
+    _announce(f"fp8 query products (fp8_qk=1, kv_reuse {kv_reuse}): lengths {lengths}, fused step then two calls")
     q, k, v = synth.prefill_batch(wl, 0, lengths)
     c = GpuCache(p, 3)
     c.k_scale.fill_(0.05)

@@ -17,6 +17,11 @@ Which kernels each case reaches (csrc names):
   latent 576, w = 16         the four-wave 576-wide score passes
   latent fp8                 fp8 latent assembly (given and data scales),
                              decode_mla<fp8>
+  *-stream                   kv_reuse = SNAP_KV_STREAM: the streaming-load
+                             instantiations of decode_mfma (bf16, fp8),
+                             decode_mla_lds and decode_mla<fp8>, which the
+                             default hint picks only for calls of 128 MiB and
+                             more (the full-size tests)
 
 Every case prints what names it before touching the GPU.
 """
@@ -64,6 +69,13 @@ CASES = {
     "latent-fp8-given": (synth.small(_LAT, kv_dtype="fp8"), {}, [6000, 2500], [2, 0], 3, 80, 8, torch.bfloat16),
     "latent-fp8-amax": (synth.small(_LAT, kv_dtype="fp8"), {"fp8_scales": snap.SNAP_FP8_SCALES_AMAX},
                         [5000, 700], [1, 2], 3, 80, 8, torch.bfloat16),
+    "gqa-d128-bf16-stream": (synth.small(_G4, d_qk=128, d_v=128), {"kv_reuse": snap.SNAP_KV_STREAM},
+                             [3001, 800], [1, 0], 2, 40, 2, torch.bfloat16),
+    "gqa-d128-fp8-stream": (synth.small(_G4, d_qk=128, d_v=128, kv_dtype="fp8"), {"kv_reuse": snap.SNAP_KV_STREAM},
+                            [2700, 1300], [0, 2], 3, 40, 2, torch.bfloat16),
+    "latent-576-stream": (_LAT, {"kv_reuse": snap.SNAP_KV_STREAM}, [5000, 2100], [1, 0], 2, 80, 8, torch.bfloat16),
+    "latent-fp8-stream": (synth.small(_LAT, kv_dtype="fp8"), {"kv_reuse": snap.SNAP_KV_STREAM}, [6000, 2500],
+                          [0, 2], 3, 80, 8, torch.bfloat16),
 }
 
 
