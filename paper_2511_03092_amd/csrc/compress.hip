@@ -52,7 +52,11 @@ struct ScoreLane {
 // y is formed as the rounded product yh plus its exact error and the part of
 // scale*log2(e) that fp32 s2 dropped; that small remainder enters to first
 // order, 2^(yh + yl - c) = 2^(yh - c) * (1 + yl*ln2), folded into the row factor.
+// No contraction here: fused into fma(acc, s2, -c), yh - c would no longer
+// carry the rounding of yh that yl corrects, and for c != 0 that error would
+// be counted twice.
 __device__ __forceinline__ float weight(float acc, float s2, float s2lo, float c, float inv, float invl) {
+#pragma clang fp contract(off)
   const float yh = acc * s2;
   float yl = fmaf(acc, s2, -yh);
   yl = fmaf(acc, s2lo, yl);

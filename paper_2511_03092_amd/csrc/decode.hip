@@ -1017,9 +1017,17 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   float pr[kCombineRegChunks];
 #pragma unroll
   for (int c = 0; c < kCombineRegChunks; ++c) pr[c] = c < nreg ? part[(size_t)c * a.dv] : 0.f;
+  // the (m, l) of this thread's chunks tid, tid + 128, ... are loaded once
   const float2* ml = a.ml + (size_t)bh * a.n_chunks;
+  constexpr int kMlPerThread = kMaxChunks / kCombineThreads;
+  float2 mlv[kMlPerThread];
   float M = -INFINITY;
-  for (int c = tid(); c < a.n_chunks; c += nthreads()) M = fmaxf(M, ml[c].x);
+#pragma unroll
+  for (int i = 0; i < kMlPerThread; ++i) {
+    const int c = tid() + kCombineThreads * i;
+    mlv[i] = c < a.n_chunks ? ml[c] : make_float2(-INFINITY, 0.f);
+    M = fmaxf(M, mlv[i].x);
+  }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   if (lane == 0) red[wave] = M;
@@ -1028,10 +1036,12 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
   for (int i = 1; i < kCombineThreads / 64; ++i) M = fmaxf(M, red[i]);
   __syncthreads();
   float ws = 0.f;
-  for (int c = tid(); c < a.n_chunks; c += nthreads()) {
-    float2 v = ml[c];
-    float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : fast_exp2(v.x - M);
-    wts[c] = wc;
+#pragma unroll
+  for (int i = 0; i < kMlPerThread; ++i) {
+    const int c = tid() + kCombineThreads * i;
+    const float2 v = mlv[i];
+    const float wc = (v.x == -INFINITY || M == -INFINITY) ? 0.f : fast_exp2(v.x - M);
+    if (c < a.n_chunks) wts[c] = wc;
     ws += wc * v.y;
   }
   ws = warp_sum(ws);
