@@ -31,6 +31,7 @@ import sys
 import time
 
 DEFAULT_WORKLOAD = "mla-8head-61layer-b16-128k"
+KV_REUSE = {"auto": 0, "stream": 1, "keep": 2}  # snap_kv_reuse
 DEFAULT_PREFILL_WORKLOAD = "llama8b-1layer-32k"
 HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -184,6 +185,8 @@ def parse():
                          "(snap_params.fp8_qk)")
     ap.add_argument("--overlap", action="store_true",
                     help="continuous batching: run each step's compression and decode on two streams at once")
+    ap.add_argument("--kv-reuse", choices=["auto", "stream", "keep"], default="auto",
+                    help="decode load hint (snap_params.kv_reuse): auto streams calls of 128 MiB and more")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
     return ap.parse_args()
@@ -218,7 +221,8 @@ def main():
     torch.cuda.set_device(dev)
     DT = {"f32": snap.SNAP_F32, "bf16": snap.SNAP_BF16, "fp8": snap.SNAP_FP8_E4M3}
     p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
-                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype])
+                    wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype],
+                    kv_reuse=KV_REUSE[args.kv_reuse])
     n = wl.batch
     lengths = synth.draw_lengths(wl, 0, n)
     max_len = max(lengths)
@@ -364,7 +368,7 @@ def main():
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "decode_steps": dsteps,
                    "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
-                   "kv_dtype": wl.kv_dtype},
+                   "kv_dtype": wl.kv_dtype, "kv_reuse": args.kv_reuse},
         "decode_step_ms_per_call": round(dec_ms, 4),
         "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(n / (decode_ms_per_token_step * 1e-3), 1) if dec_ms > 0 else 0.0,
@@ -417,7 +421,7 @@ def run_cb(args, wl):
     p = snap.Params(wl.n_q_heads, wl.n_kv_heads, wl.d_qk, wl.d_v, wl.sink, wl.recent, wl.topk, wl.obs_window,
                     wl.pool_kernel, wl.pool, wl.norm, wl.v_in_k, DT[wl.in_dtype], DT[wl.kv_dtype],
                     fp8_scales=snap.SNAP_FP8_SCALES_AMAX if args.fp8_scales_from_data else snap.SNAP_FP8_SCALES_GIVEN,
-                    fp8_qk=1 if args.fp8_qk else 0)
+                    fp8_qk=1 if args.fp8_qk else 0, kv_reuse=KV_REUSE[args.kv_reuse])
     B = p.budget
     Lmax = wl.max_len
     n_steps = args.warmup + args.steps
@@ -567,7 +571,7 @@ def run_cb(args, wl):
                            "step of the other slots",
                    "fp8_scales": "amax/448 of the kept rows, set by snap_compress" if args.fp8_scales_from_data
                    else "amax/448 of the layer's prompt bank, set by the harness",
-                   "fp8_qk": bool(args.fp8_qk)},
+                   "fp8_qk": bool(args.fp8_qk), "kv_reuse": args.kv_reuse},
         "decode_step_ms_per_call": round(dec_ms, 4),
         "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(nd / (dec_ms * layers * 1e-3), 1) if dec_ms > 0 else 0.0,
