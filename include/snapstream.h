@@ -80,7 +80,9 @@ typedef enum {
                                 tokens appended later saturate at +-448 codes */
 } snap_fp8_scales;
 
-/* How decode reads the cache rows (a load hint; results are the same). */
+/* How decode reads the cache rows: a load hint.  Results agree to rounding
+ * (under streaming loads the bf16 GQA kernel adds the dot products' 8-element
+ * pieces in another order; the other kernels give the same bits). */
 typedef enum {
   SNAP_KV_AUTO = 0,   /* streaming when the call's cache rows at the full
                          budget reach 128 MiB, cached loads otherwise          */
