@@ -130,3 +130,47 @@ def test_fp8_query_products(kv_reuse):
                         stats=stats)
     print(f"  max abs err vs oracle with the fp8 query: {max(err, err2):.3e}; "
           f"deviation from the exact query: {stats['exact_query_dev']:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("kind", ["gqa-bf16", "gqa-fp8", "latent-bf16", "latent-fp8"])
+def test_load_hint_keeps_results(kind):
+    """snap_params.kv_reuse only changes how the cache rows are loaded: the
+    same decode call with ordinary (SNAP_KV_KEEP) and streaming
+    (SNAP_KV_STREAM) loads gives the same bits, except the bf16 GQA kernel,
+    which adds the dot products' pieces in another order under streaming
+    loads (outputs then agree to a few bf16 ulps)."""
+    if kind.startswith("gqa"):
+        wl = synth.small(GQA, kv_dtype="fp8") if kind == "gqa-fp8" else GQA
+        lengths = [2900, 40, 1200]
+    else:
+        wl = synth.small(synth.WORKLOADS["mla-8head-61layer-b16-128k"], recent=64, topk=1000,
+                         kv_dtype="fp8" if kind == "latent-fp8" else "bf16")
+        lengths = [3000, 70, 1500]
+    p = params_of(wl)
+    _announce(f"load hint keep vs stream: {kind}, lengths {lengths}")
+    q, k, v = synth.prefill_batch(wl, 0, lengths)
+    c = GpuCache(p, 3)
+    if c.k_scale is not None:
+        c.k_scale.fill_(0.05)
+        if c.v_scale is not None:
+            c.v_scale.fill_(0.05)
+    gpu_compress(p, c, q, k, v, lengths, [0, 1, 2], debug=False)
+    sl = torch.tensor([0, 1, 2], dtype=torch.int32, device="cuda")
+    positions = [int(x) for x in c.pos.cpu()]
+    qd, _, _ = synth.decode_inputs(wl, 0, 0, positions, device="cuda")
+    outs = {}
+    for hint in (snap.SNAP_KV_KEEP, snap.SNAP_KV_STREAM):
+        ph = params_of(wl, kv_reuse=hint)
+        out = torch.zeros((3, p.n_q_heads, p.d_v), dtype=torch.float32, device="cuda")
+        ws = snap.workspace(snap.snap_decode_workspace(ph, 3))
+        snap.snap_decode_attn(ph, c.c(), c.pos, c.n_topk, sl, qd, out, ws)
+        torch.cuda.synchronize()
+        outs[hint] = out
+    a, b = outs[snap.SNAP_KV_KEEP], outs[snap.SNAP_KV_STREAM]
+    assert torch.isfinite(a).all()
+    if kind == "gqa-bf16":
+        diff = float((a - b).abs().max())
+        print(f"  max abs difference: {diff:.3e}", flush=True)
+        assert diff <= 1e-4 * max(1.0, float(a.abs().max()))
+    else:
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
