@@ -79,6 +79,12 @@ def load(path: str) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2511_03092_amd.build` "
                           "(there is no fallback implementation)")
+    # torch first: its HIP runtime is then the process's libamdhip64.so.7, and
+    # the library binds to that same runtime (the one that owns the device
+    # memory passed in).  Loaded before torch, the library would bring in the
+    # system's runtime beside torch's, and its launches would not see torch's
+    # device state.
+    import torch  # noqa: F401
     L = ctypes.CDLL(path)
     P, vp, i32, sz = ctypes.POINTER(SnapParams), ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     C = ctypes.POINTER(SnapCache)

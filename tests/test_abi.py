@@ -284,3 +284,19 @@ def test_launch_grid_limits():
     assert st == snap.SNAP_ERR_UNSUPPORTED  # 4096 x 32 query heads
     st = L.snap_prefill_attn(ctypes.byref(p.c()), 64, FAKE, 1 << 28, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 62, None)
     assert st == snap.SNAP_ERR_UNSUPPORTED  # 512 groups x 2^23 position blocks
+
+
+def test_library_binds_to_torchs_hip_runtime():
+    """Loaded before anything imported torch, the library still ends up on
+    torch's HIP runtime (the one that owns the device memory the binding
+    passes in): one libamdhip64 in the process, not two."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "import paper_2511_03092_amd as snap\n"
+            "snap.lib()\n"
+            "print(sorted(set(l.split()[-1] for l in open('/proc/self/maps') if 'amdhip64' in l)))\n") % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    maps = eval(out.stdout.strip().splitlines()[-1])
+    assert len(maps) == 1 and "torch" in maps[0], maps
