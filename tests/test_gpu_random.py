@@ -91,5 +91,57 @@ def test_random_config(i):
           f"in {wl.in_dtype} cache {wl.kv_dtype} fp8_scales {p.fp8_scales} given {given} window {p.obs_window} "
           f"pool {p.pool}/{p.pool_kernel} norm {p.norm} sink {p.sink} recent {p.recent} topk {p.topk} "
           f"kv_reuse {p.kv_reuse} out {out_dtype} lengths {lengths} -> slots {slots} of {n_slots}", flush=True)
+    # even steps: snap_cache_append + snap_decode_attn; odd steps: snap_decode_step
     run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, TOL[wl.kv_dtype], check_every=3, fp8_scales=given,
-             near_rtol=near, salt=i)
+             near_rtol=near, salt=i, fused="alt")
+
+
+N_PREFILL = 10
+
+
+def draw_prefill(i: int):
+    """Prefill case i: a configuration snap_prefill accepts (bf16 inputs, d 64
+    or 128 with a separate V, G in 1, 2, 4, 8, 16) with a bf16 or fp8 cache."""
+    r = random.Random(SEED * 1000 + 500 + i)
+    d = r.choice([64, 128])
+    hkv = r.choice([1, 2])
+    while True:
+        G = r.choice([1, 2, 4, 8, 16])
+        w = r.choice([1, 4, 16, 32])
+        if G * w <= 256:
+            break
+    sink, recent = r.randint(0, 8), r.randint(1, 48)
+    topk = r.choice([0, r.randint(1, 300)])
+    kv = r.choice(["bf16", "fp8"])
+    batch = r.randint(1, 3)
+    lengths = [r.choice([r.randint(1, sink + recent + 3), r.randint(100, 1200)]) for _ in range(batch)]
+    n_slots = batch + r.randint(0, 1)
+    slots = r.sample(range(n_slots), batch)
+    wl = synth.Workload(f"rand-pf-{i}", 200 + i, G * hkv, hkv, d, d, False, sink, recent, topk, w,
+                        r.choice([1, 3, 7]), "bf16", kv, layers=1, batch=batch, length=None, length_range=(1, 1200),
+                        decode_steps=0, rope=True, plant_frac=0.01, pool=r.choice([synth.POOL_MAX, synth.POOL_AVG]),
+                        norm=r.choice([synth.NORM_CAND, synth.NORM_ROW]))
+    over = {"fp8_scales": snap.SNAP_FP8_SCALES_AMAX} if kv == "fp8" else {}
+    near = NEAR_RTOL_ONE_ROW if G * w < 8 else NEAR_RTOL
+    return wl, over, lengths, slots, n_slots, near
+
+
+def test_random_prefill_configs_are_accepted():
+    for i in range(N_PREFILL):
+        wl, over, lengths, slots, n_slots, _ = draw_prefill(i)
+        p = params_of(wl, **over)
+        assert snap.snap_prefill_workspace(p, len(lengths), max(lengths)) > 0, (i, wl)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("i", range(N_PREFILL))
+def test_random_prefill_config(i):
+    """snap_prefill on a random accepted configuration: the attention output
+    of every position and the fused compression against the oracle."""
+    from test_gpu_prefill import _run
+    wl, over, lengths, slots, n_slots, near = draw_prefill(i)
+    p = params_of(wl, **over)
+    print(f"\n[case] random prefill {i}: Hq {p.n_q_heads} Hkv {p.n_kv_heads} d {p.d_qk} cache {wl.kv_dtype} "
+          f"window {p.obs_window} pool {p.pool}/{p.pool_kernel} norm {p.norm} sink {p.sink} recent {p.recent} "
+          f"topk {p.topk} lengths {lengths} -> slots {slots} of {n_slots}", flush=True)
+    _run(wl, p, lengths, slots=slots, n_slots=n_slots, near_rtol=near)
