@@ -22,7 +22,7 @@ import paper_2511_03092_amd as snap
 import synth
 from snaphelp import NEAR_RTOL, NEAR_RTOL_ONE_ROW, TOL, params_of, run_case
 
-N_CASES = 24
+N_CASES = 64
 SEED = 2511
 
 
@@ -96,7 +96,7 @@ def test_random_config(i):
              near_rtol=near, salt=i, fused="alt")
 
 
-N_PREFILL = 10
+N_PREFILL = 16
 
 
 def draw_prefill(i: int):
