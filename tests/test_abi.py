@@ -300,3 +300,23 @@ def test_library_binds_to_torchs_hip_runtime():
     assert out.returncode == 0, out.stderr
     maps = eval(out.stdout.strip().splitlines()[-1])
     assert len(maps) == 1 and "torch" in maps[0], maps
+
+
+def test_header_compiles_and_links_as_c(tmp_path):
+    """tests/c_abi_host.c, a plain C11 caller, compiles against the header
+    with -Wall -Werror, links the built library and gets workspace sizes and
+    a refused parameter back without a GPU."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    exe = tmp_path / "c_abi_host"
+    libdir = os.path.dirname(snap.LIB_PATH)
+    r = subprocess.run([cc, "-std=c11", "-Wall", "-Wextra", "-Werror", "-I", os.path.join(ROOT, "include"),
+                        os.path.join(ROOT, "tests", "c_abi_host.c"), "-L", libdir, "-lsnapstream",
+                        "-Wl,-rpath," + libdir, "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stdout + out.stderr
+    assert "status 1 invalid argument" in out.stdout and "pool_kernel" in out.stdout, out.stdout
