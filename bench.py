@@ -185,6 +185,9 @@ def parse():
                          "(snap_params.fp8_qk)")
     ap.add_argument("--overlap", action="store_true",
                     help="continuous batching: run each step's compression and decode on two streams at once")
+    ap.add_argument("--compress-streams", type=int, default=1, metavar="K",
+                    help="continuous batching: the new prompt's per-layer compress calls over K streams "
+                         "(layers are independent; each stream has its own workspace)")
     ap.add_argument("--kv-reuse", choices=["auto", "stream", "keep"], default="auto",
                     help="decode load hint (snap_params.kv_reuse): auto streams calls of 128 MiB and more")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -450,17 +453,33 @@ def run_cb(args, wl):
     lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
     # the decoded slots of the step that retires slot r: every slot but r
     live = [torch.tensor([x for x in range(S) if x != r], dtype=torch.int32, device=dev) for r in range(S)]
-    wsc = snap.workspace(snap.snap_compress_workspace(p, 1, Lmax), dev)
+    KC = max(1, args.compress_streams)
+    wscs = [snap.workspace(snap.snap_compress_workspace(p, 1, Lmax), dev) for _ in range(KC)]
     wsd = snap.workspace(snap.snap_decode_workspace(p, nd), dev)
     out = torch.empty((nd, wl.n_q_heads, wl.d_v), dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
+    side = [torch.cuda.Stream() for _ in range(KC)] if KC > 1 else []
 
-    def compress(i, slot, sp):
+    def compress(i, slot, st):
+        # one prompt into `slot` for every layer, ordered on stream st (with
+        # --compress-streams K the layers run on K side streams that start
+        # after, and end before, st's work at this point)
+        if KC > 1:
+            e = torch.cuda.Event()
+            e.record(st)
+            for x in side:
+                x.wait_event(e)
         for l in range(layers):
             kb, vb = banks[l]
+            sp = side[l % KC].cuda_stream if KC > 1 else st.cuda_stream
             snap.snap_compress(p, caches[l][4], pos, ntop, slot_ids[slot:slot + 1], lens[i:i + 1],
-                               obsq[l][i:i + 1], kb, vb, wsc, stream=sp)
+                               obsq[l][i:i + 1], kb, vb, wscs[l % KC], stream=sp)
+        if KC > 1:
+            for x in side:
+                e = torch.cuda.Event()
+                e.record(x)
+                st.wait_event(e)
 
     def decode(t, retired, sp):
         for l in range(layers):
@@ -470,7 +489,7 @@ def run_cb(args, wl):
         snap.snap_advance(pos, live[retired], stream=sp)
 
     for r in range(S):  # fill every slot
-        compress(r, r, sptr)
+        compress(r, r, stream)
     torch.cuda.synchronize()
     t_setup = time.time() - t_setup
     if args.copy_calibration:
@@ -509,7 +528,7 @@ def run_cb(args, wl):
         if overlap and prev_d is not None:
             s_c.wait_event(prev_d)
         c0 = ev(s_c)
-        compress(i, r, s_c.cuda_stream)
+        compress(i, r, s_c)
         prev_c_next = ev(s_c)
         if overlap and prev_c is not None:
             s_d.wait_event(prev_c)
@@ -571,7 +590,7 @@ def run_cb(args, wl):
                            "step of the other slots",
                    "fp8_scales": "amax/448 of the kept rows, set by snap_compress" if args.fp8_scales_from_data
                    else "amax/448 of the layer's prompt bank, set by the harness",
-                   "fp8_qk": bool(args.fp8_qk), "kv_reuse": args.kv_reuse},
+                   "fp8_qk": bool(args.fp8_qk), "kv_reuse": args.kv_reuse, "compress_streams": KC},
         "decode_step_ms_per_call": round(dec_ms, 4),
         "decode_step_hbm_gbps": round(dec_gbps, 1),
         "decode_only_tok_s": round(nd / (dec_ms * layers * 1e-3), 1) if dec_ms > 0 else 0.0,
