@@ -113,6 +113,12 @@ def device_code_sha256(lib_path: str, kernels: str):
     return hashlib.sha256(b"".join(parts)).hexdigest() if parts else None
 
 
+def seed_rule(wl):
+    """How every synthetic input of the run is seeded (all are drawn from
+    these counters alone, so a run is reproducible from the workload name)."""
+    return {"cfg_id": wl.cfg_id, "rule": "synth.seed_of(cfg_id, layer, slot, purpose, step)"}
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the roofline kernel from the committed counter
     runs (profiles/traffic.json, keyed by workload; the prefill attention's
@@ -367,7 +373,7 @@ def main():
         "dtype": "bf16" if wl.in_dtype == "bf16" else "f32",
         "data": "synthetic",
         "launch": "hip_graph" if args.graph else "eager",
-        "config": {"workload": wl.name, "layers": layers, "sequences": n, "prompt_lengths": lengths,
+        "config": {"workload": wl.name, "seeds": seed_rule(wl), "layers": layers, "sequences": n, "prompt_lengths": lengths,
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "decode_steps": dsteps,
                    "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
@@ -581,7 +587,7 @@ def run_cb(args, wl):
         "dtype": "bf16",
         "data": "synthetic",
         "launch": "eager, compression and decode on two streams" if overlap else "eager, one stream",
-        "config": {"workload": wl.name, "layers": layers, "slots": S, "decoded_per_step": nd,
+        "config": {"workload": wl.name, "seeds": seed_rule(wl), "layers": layers, "slots": S, "decoded_per_step": nd,
                    "prompt_length_range": list(wl.length_range), "prompt_bank_tokens": Lmax,
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
                    "obs_window": wl.obs_window, "pool_kernel": wl.pool_kernel, "q_heads": wl.n_q_heads,
@@ -733,7 +739,7 @@ def run_prefill(args, wl):
         "dtype": "bf16",
         "data": "synthetic",
         "launch": "eager",
-        "config": {"workload": wl.name, "layers": layers, "sequences": n, "prompt_lengths": lengths,
+        "config": {"workload": wl.name, "seeds": seed_rule(wl), "layers": layers, "sequences": n, "prompt_lengths": lengths,
                    "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "d_qk": wl.d_qk, "d_v": wl.d_v,
                    "sink": wl.sink, "recent": wl.recent, "topk": wl.topk, "obs_window": wl.obs_window,
                    "pool_kernel": wl.pool_kernel, "kv_dtype": wl.kv_dtype},
