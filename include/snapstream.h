@@ -31,7 +31,11 @@
  *    faulting: lengths are clamped to [0, max_len]; a slot id outside
  *    [0, n_slots) makes the call skip that sequence.
  *  - Inputs must not alias the cache.  Calls on disjoint buffers may run
- *    concurrently on different streams.
+ *    concurrently on different streams.  One exception to disjointness:
+ *    snap_compress / snap_prefill calls of different layers for the same
+ *    prompt may run concurrently although they share that slot's pos and
+ *    n_topk entries, since those calls only write them, with the same values
+ *    (L and min(K, |C|)).
  *  - Batch limits of the launch grids: n_seq * n_kv_heads <= 65535
  *    (snap_compress, snap_prefill, snap_prefill_attn) and n * n_q_heads <=
  *    65535 (snap_decode_attn, snap_decode_step); larger calls return
