@@ -27,6 +27,7 @@ import argparse
 import json
 import math
 import os
+import subprocess
 import sys
 import time
 
@@ -198,11 +199,12 @@ def parse():
                     help="decode load hint (snap_params.kv_reuse): auto streams calls of 128 MiB and more")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the run, copy BYTES device-to-device once (a reference for HBM counters)")
+    ap.add_argument("--no-others", action="store_true",
+                    help="the default run: skip the short runs of the other workloads after the headline one")
     return ap.parse_args()
 
 
-def main():
-    args = parse()
+def main(args):
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the hot path shards by "
               "KV head or by slot with no exchange; see the design notes). Run with --gpus 1.",
@@ -397,7 +399,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, p, lengths, n, layers, dsteps, n * dsteps, value)
-    print(json.dumps(res), flush=True)
+    return res
 
 
 def run_cb(args, wl):
@@ -913,5 +915,64 @@ def cpu_baseline(wl, p, comp_lengths, dec_seqs, layers, dsteps, tokens, gpu_valu
             "gpu_over_cpu": float(f"{gpu_value / valT:.4g}")}
 
 
+# The other workloads, timed after the headline one by the default run (each
+# in a child process of its own, once the headline run's memory is freed), so
+# that one plain `python3 bench.py` measures every configuration: the GQA
+# batch, continuous batching, the launch-bound one-layer decode (as a HIP
+# graph) and the prefill attention + fused compression.
+OTHER_RUNS = [
+    ["--workload", "llama8b-32layer-b8-128k", "--steps", "1", "--warmup", "1"],
+    ["--workload", "cb-fp8-llama8b-32slot"],
+    ["--workload", "llama8b-1layer-32k", "--graph"],
+    ["--prefill"],
+]
+OTHER_KEYS = ["value", "unit", "ms_per_step", "steps", "warmup", "launch", "decode_step_ms_per_call",
+              "decode_step_hbm_gbps", "compress_ms_per_layer_call", "compress_ms_per_seq_layer",
+              "attention_ms_per_layer_call", "prefill_ms_per_layer_call"]
+
+
+def wants_others(args) -> bool:
+    return (args.workload is None and not args.prefill and not args.no_others and args.layers is None
+            and args.decode_steps is None and not args.copy_calibration)
+
+
+def run_others(timeout_s: float = 300.0):
+    out = []
+    for extra in OTHER_RUNS:
+        cmd = [sys.executable, os.path.abspath(__file__), "--no-cpu-baseline", "--no-others"] + extra
+        print("[bench] other workload:", " ".join(extra), file=sys.stderr, flush=True)
+        t0 = time.time()
+        rec = {"args": " ".join(extra)}
+        try:
+            r = subprocess.run(cmd, capture_output=True, text=True, timeout=timeout_s)
+            lines = [x for x in r.stdout.splitlines() if x.startswith("{")]
+            if r.returncode != 0 or not lines:
+                rec["error"] = f"exit status {r.returncode}"
+                rec["stderr_tail"] = r.stderr[-400:]
+            else:
+                d = json.loads(lines[-1])
+                rec["workload"] = d["config"]["workload"]
+                rec.update({k: d[k] for k in OTHER_KEYS if k in d})
+                rf = d.get("roofline") or {}
+                rec["roofline"] = {k: rf[k] for k in ("bound", "achieved", "peak", "unit", "frac") if k in rf}
+        except subprocess.TimeoutExpired:
+            rec["error"] = f"no result within {timeout_s:.0f} s"
+        rec["wall_s"] = round(time.time() - t0, 1)
+        out.append(rec)
+    return out
+
+
 if __name__ == "__main__":
-    main()
+    args = parse()
+    others = wants_others(args)  # before main() fills in the default workload
+    res = main(args)
+    if res is not None:  # the decode driver's line (the other drivers print their own)
+        if others:
+            import gc
+
+            import torch
+            gc.collect()
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            res["other_workloads"] = run_others()
+        print(json.dumps(res), flush=True)
