@@ -164,6 +164,10 @@ def copy_calibration(torch, nbytes, dev):
     del src, dst
 
 
+# continuous batching: the new prompt's per-layer compressions run on this many
+# streams (measured 3405 tok/s with 1, 4250 with 2, 4070 with 4, 4337 with 8)
+DEFAULT_COMPRESS_STREAMS = 2
+
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 
@@ -192,9 +196,10 @@ def parse():
                          "(snap_params.fp8_qk)")
     ap.add_argument("--overlap", action="store_true",
                     help="continuous batching: run each step's compression and decode on two streams at once")
-    ap.add_argument("--compress-streams", type=int, default=1, metavar="K",
+    ap.add_argument("--compress-streams", type=int, default=None, metavar="K",
                     help="continuous batching: the new prompt's per-layer compress calls over K streams "
-                         "(layers are independent; each stream has its own workspace)")
+                         f"(default {DEFAULT_COMPRESS_STREAMS}; layers are independent; each stream has its own "
+                         "workspace; 1 runs them in order on the step's stream)")
     ap.add_argument("--kv-reuse", choices=["auto", "stream", "keep"], default="auto",
                     help="decode load hint (snap_params.kv_reuse): auto streams calls of 128 MiB and more")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -461,7 +466,7 @@ def run_cb(args, wl):
     lens = torch.tensor(lengths, dtype=torch.int32, device=dev)
     # the decoded slots of the step that retires slot r: every slot but r
     live = [torch.tensor([x for x in range(S) if x != r], dtype=torch.int32, device=dev) for r in range(S)]
-    KC = max(1, args.compress_streams)
+    KC = max(1, DEFAULT_COMPRESS_STREAMS if args.compress_streams is None else args.compress_streams)
     wscs = [snap.workspace(snap.snap_compress_workspace(p, 1, Lmax), dev) for _ in range(KC)]
     wsd = snap.workspace(snap.snap_decode_workspace(p, nd), dev)
     out = torch.empty((nd, wl.n_q_heads, wl.d_v), dtype=torch.bfloat16, device=dev)
@@ -588,7 +593,9 @@ def run_cb(args, wl):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "launch": "eager, compression and decode on two streams" if overlap else "eager, one stream",
+        "launch": ("eager, compression and decode on two streams" if overlap else
+                   "eager, one stream" if KC == 1 else
+                   f"eager, the layers' compressions over {KC} streams, then the decode step"),
         "config": {"workload": wl.name, "seeds": seed_rule(wl), "layers": layers, "slots": S, "decoded_per_step": nd,
                    "prompt_length_range": list(wl.length_range), "prompt_bank_tokens": Lmax,
                    "budget": B, "sink": wl.sink, "recent": wl.recent, "topk": wl.topk,
