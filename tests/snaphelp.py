@@ -1,7 +1,7 @@
 """Helpers shared by the GPU parity tests: run the HIP path through the C ABI
 on seeded synthetic inputs and check it against the fp64 oracle.
 
-Acceptance rules (the benchmark spec's bar):
+Acceptance rules:
   * kept index sets: exact, except swaps between candidates whose oracle
     pooled scores lie within 1e-6 (relative) of the K-th largest score;
   * cache bytes: sinks, ring rows and every kept row are exact copies of the
