@@ -38,8 +38,8 @@ struct ScoreArgs {
   int Hq, Hkv, G, w, max_len, sink, recent, norm;
   int rows, rows_pad, key_chunk, n_kchunks;
   float scale;   // softmax scale
-  float scale2;     // scale * log2(e) rounded to fp32: logits in log2 units
-  float scale2_lo;  // scale * log2(e) - scale2
+  float scale2;     // scale * log2(e) rounded to fp32 toward zero: logits in log2 units
+  float scale2_lo;  // scale * log2(e) - scale2, > 0 (see split_scale2)
 };
 
 struct ScoreLane {
@@ -134,9 +134,9 @@ __device__ __forceinline__ void score_mma_sb(const unsigned char* __restrict__ k
   }
 }
 
-// Softmax arithmetic of sub-block sb from its products: STATS keeps the scaled
-// logits in xv for score_stats_tile; COLSUM writes this wave's column sums of
-// the normalised weights to colbuf.
+// Softmax arithmetic of sub-block sb from its products: STATS keeps the
+// products (masked ones at -inf) in xv for score_stats_tile; COLSUM writes this
+// wave's column sums of the normalised weights to colbuf.
 template <int NW, bool COLSUM, int TK>
 __device__ __forceinline__ void score_epi_sb(const ScoreArgs& a, const f32x4 (&acc)[2], float* colbuf,
                                              const ScoreLane& sl, int t0, int c1, bool interior, int sb, int wave,
@@ -146,10 +146,12 @@ __device__ __forceinline__ void score_epi_sb(const ScoreArgs& a, const f32x4 (&a
   const int key = sb * 16 + l16;
   const int j = t0 + key;
   if (!COLSUM) {
+    // the raw products: score_stats_tile forms each exponent from them with
+    // the full scale (s2 + s2lo), as the column-sum weights do
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) xv[rb][e][sb] = acc[rb][e] * s2;
+      for (int e = 0; e < 4; ++e) xv[rb][e][sb] = acc[rb][e];
     if (!interior) {
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
@@ -179,9 +181,18 @@ __device__ __forceinline__ void score_epi_sb(const ScoreArgs& a, const f32x4 (&a
   }
 }
 
-// STATS: fold one tile's scaled logits into the running row max / sum.
+// STATS: fold one tile's products into the running row max / sum (log2
+// units).  The reference mn is the rounded max of acc * s2; each term's
+// exponent acc * (s2 + s2lo) - mn is formed with two fused steps, so the row
+// sum carries neither the rounding of acc * s2 nor the part of the scale that
+// fp32 s2 drops -- the same logits the column-sum weights use, whose sum it
+// normalises.  s2lo > 0 keeps a masked -inf product at -inf.
+__device__ __forceinline__ float stats_term(float x, float s2, float s2lo, float mn) {
+  return fast_exp2(fmaf(x, s2lo, fmaf(x, s2, -mn)));
+}
 template <int TK>
-__device__ __forceinline__ void score_stats_tile(ScoreLane& sl, const float (&xv)[2][4][TK / 16]) {
+__device__ __forceinline__ void score_stats_tile(ScoreLane& sl, const float (&xv)[2][4][TK / 16], float s2,
+                                                 float s2lo) {
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
@@ -193,13 +204,14 @@ __device__ __forceinline__ void score_stats_tile(ScoreLane& sl, const float (&xv
       } else {
         mt = fmaxf(x[0], x[1]);
       }
-      mn = fmaxf(sl.rm[rb][e], mt);
+      mn = fmaxf(sl.rm[rb][e], mt * s2);
       if (mn == -INFINITY) continue;
       float z = sl.rz[rb][e] * fast_exp2(sl.rm[rb][e] - mn);
       if constexpr (TK == 64) {
-        z += (fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) + (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn));
+        z += (stats_term(x[0], s2, s2lo, mn) + stats_term(x[1], s2, s2lo, mn)) +
+             (stats_term(x[2], s2, s2lo, mn) + stats_term(x[3], s2, s2lo, mn));
       } else {
-        z += fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn);
+        z += stats_term(x[0], s2, s2lo, mn) + stats_term(x[1], s2, s2lo, mn);
       }
       sl.rz[rb][e] = z;
       sl.rm[rb][e] = mn;
@@ -221,7 +233,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, const unsigned ch
     score_mma_sb<In, KSTEPS, TK>(ktile, qf, qlds, sb, wave, lane, wave_has_rows, acc);
     score_epi_sb<NW, COLSUM, TK>(a, acc, colbuf, sl, t0, c1, interior, sb, wave, lane, xv);
   }
-  if (!COLSUM) score_stats_tile<TK>(sl, xv);
+  if (!COLSUM) score_stats_tile<TK>(sl, xv, a.scale2, a.scale2_lo);
 }
 
 // Column sums of one tile across the NW waves (fixed order), written to A.
@@ -1388,6 +1400,18 @@ __global__ __launch_bounds__(256) void assemble(AssembleArgs a) {
 // ============================================================ host side
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// scale * log2(e) as hi + lo: hi the fp32 value rounded toward zero, lo the
+// rest, strictly positive (a tiny positive value when hi is exact, where it
+// changes no finite product): a masked -inf product times lo stays -inf.
+void split_scale2(float scale, float& hi, float& lo) {
+  const double x = (double)scale * 1.4426950408889634074;
+  float h = (float)x;
+  if ((double)h > x) h = nextafterf(h, 0.f);
+  const float l = (float)(x - (double)h);
+  hi = h;
+  lo = l > 0.f ? l : 1e-30f;
+}
+
 SNAP_DEBUG_READER(debug_flags_compress)
 
 Geometry compress_geometry(const snap_params& p, int n_seq, int max_len) {
@@ -1530,8 +1554,7 @@ snap_status launch_compress(const snap_params& p, const snap_cache& c, int32_t* 
   sa.key_chunk = geo.key_chunk;
   sa.n_kchunks = geo.n_kchunks;
   sa.scale = scale;
-  sa.scale2 = (float)((double)scale * 1.4426950408889634074);
-  sa.scale2_lo = (float)((double)scale * 1.4426950408889634074 - (double)sa.scale2);
+  split_scale2(scale, sa.scale2, sa.scale2_lo);
   const bool bf = p.in_dtype == SNAP_BF16;
   hipError_t e;
   // With no selected rows (StreamingLLM alone) the cache is sinks and ring

@@ -40,7 +40,8 @@ struct PrefillArgs {
   int Hq, Hkv, G, max_len, ld_vt, w, sink, recent, norm, rows, rows_pad, want_stats;
   int P;               // query positions per workgroup
   int n_qblocks, groups;  // workgroups per group (max_len / P rounded up), n_seq * Hkv
-  float scale2;        // softmax scale * log2(e), rounded to fp32
+  float scale2;        // softmax scale * log2(e) as scale2 + scale2_lo (split_scale2)
+  float scale2_lo;
 };
 
 // Query positions per workgroup for G heads per KV head: the 256 rows of a
@@ -184,10 +185,12 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
   float m[2] = {-INFINITY, -INFINITY};
   double ls[2] = {0.0, 0.0};
   // window workgroups with the candidate normaliser also keep the statistics
-  // over C = [sink, L - recent) (intersected with the causal prefix)
+  // over C = [sink, L - recent) (intersected with the causal prefix), their
+  // exponents with the full scale (s2 + s2lo) of the compression's weights
   const bool win = a.want_stats && top > L - a.w;
   const bool cand = win && a.norm == SNAP_NORM_CAND;
   const int clo = a.sink, chi = L - a.recent;
+  const float s2lo = a.scale2_lo;
   float mc[2] = {-INFINITY, -INFINITY};
   double zc[2] = {0.0, 0.0};
 
@@ -259,8 +262,12 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
           for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
+              // a select, not a branch: as a conditional sum the larger
+              // exponent made the compiler branch per element
               const int j = t0 + kb * 16 + 4 * lg + e;
-              if (j >= clo && j < chi) z += fast_exp2(fmaf(s[rb][kb][e], s2, -cn));
+              const float xs = s[rb][kb][e];
+              const float t = fast_exp2(fmaf(xs, s2lo, fmaf(xs, s2, -cn)));
+              z += (j >= clo && j < chi) ? t : 0.f;
             }
           zc[rb] = fma(zc[rb], (double)fast_exp2(mc[rb] - cn), (double)z);
           mc[rb] = cn;
@@ -433,7 +440,7 @@ snap_status launch_prefill_attn(const snap_params& p, int n_seq, const int32_t* 
   pa.rows_pad = geo.rows_pad;
   pa.want_stats = want_stats ? 1 : 0;
   pa.P = prefill_positions(G);
-  pa.scale2 = (float)((double)scale * 1.4426950408889634074);
+  split_scale2(scale, pa.scale2, pa.scale2_lo);
   pa.n_qblocks = (max_len + pa.P - 1) / pa.P;
   pa.groups = groups;
   dim3 grid(8 * ((groups + 7) / 8) * pa.n_qblocks);

@@ -182,6 +182,9 @@ struct RadixState {
   int32_t pad[3];
 };
 
+// scale * log2(e) split as hi + lo (hi: fp32 rounded toward zero; lo > 0)
+void split_scale2(float scale, float& hi, float& lo);
+
 Geometry compress_geometry(const snap_params& p, int n_seq, int max_len);
 Geometry decode_geometry(const snap_params& p, int n);
 Geometry prefill_geometry(const snap_params& p, int n_seq, int max_len);

@@ -28,10 +28,10 @@ TOL = {"f32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
 #    2e-6 of the oracle's, so the whole decision band is re-scored), so what
 #    remains is the fp32
 #    rounding of the stored score (6e-8) and the error of the rows'
-#    normalisers, which sum exponentials of fp32 logits: a row dominated by one
-#    large logit y carries up to about ln2 * |y| * 2^-23 (~1e-6 at y = 17) in
-#    its normaliser, and a candidate's score averages that over the rows that
-#    weigh it (measured at most 2.9e-7, on 32-row windows);
+#    normalisers: their terms use the same full-scale exponents as the
+#    weights, so what remains is the fp32 accumulation of the products, a few
+#    roundings of a row's largest logits, averaged over the rows that weigh a
+#    candidate (at most 3.0e-7 over 1300 random configurations);
 #  * near band -- within a factor 4 of it (fp32 score path: exp2 to 1 ulp,
 #    fp32 logits from the MFMA accumulation, the column-sum and pooling trees;
 #    ~1e-6 with w = 32, ~3e-6 with one window row, where a key's score sums
