@@ -184,12 +184,14 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
   // feeds the selection directly).
   float m[2] = {-INFINITY, -INFINITY};
   double ls[2] = {0.0, 0.0};
-  // window workgroups with the candidate normaliser also keep the statistics
-  // over C = [sink, L - recent) (intersected with the causal prefix), their
-  // exponents with the full scale (s2 + s2lo) of the compression's weights
+  // window workgroups also keep the window rows' statistics over the
+  // normaliser's domain -- C = [sink, L - recent) intersected with the
+  // causal prefix (Eq. 3), or the causal row -- with the full scale
+  // (s2 + s2lo) of the compression's weights in their exponents, which the
+  // attention's own softmax does not carry
   const bool win = a.want_stats && top > L - a.w;
-  const bool cand = win && a.norm == SNAP_NORM_CAND;
-  const int clo = a.sink, chi = L - a.recent;
+  const bool cand_norm = a.norm == SNAP_NORM_CAND;
+  const int clo = cand_norm ? a.sink : 0, chi = cand_norm ? L - a.recent : L;
   const float s2lo = a.scale2_lo;
   float mc[2] = {-INFINITY, -INFINITY};
   double zc[2] = {0.0, 0.0};
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
           for (int e = 0; e < 4; ++e)
             if (t0 + kb * 16 + 4 * lg + e > prow[rb]) s[rb][kb][e] = -INFINITY;
     }
-    if (cand) {
+    if (win) {
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
         float cm = -INFINITY;
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int j = t0 + kb * 16 + 4 * lg + e;
-            if (j >= clo && j < chi) cm = fmaxf(cm, s[rb][kb][e]);
+            cm = fmaxf(cm, (j >= clo && j < chi) ? s[rb][kb][e] : -INFINITY);
           }
         cm = lanes4_max(cm);
         const float cn = fmaxf(mc[rb], cm * s2);
@@ -367,7 +369,7 @@ __global__ __launch_bounds__(512) void prefill_attn(PrefillArgs a) {
     if (win && ii >= 0) {
       const int rho = hl[rb] * a.w + ii;
       if (lg == 0)
-        a.stats[(size_t)bg * a.rows_pad + rho] = a.norm == SNAP_NORM_CAND ? make_float2(mc[rb], zt) : make_float2(m[rb], l);
+        a.stats[(size_t)bg * a.rows_pad + rho] = make_float2(mc[rb], zt);
       uint16_t* qo = a.qobs + (((size_t)b * a.Hq + (size_t)g * a.G + hl[rb]) * a.w + ii) * D;
 #pragma unroll
       for (int t = 0; t < KS; ++t) *(u32x4*)(qo + 8 * (KS * lg + t)) = __builtin_bit_cast(u32x4, qf[rb][t]);

@@ -1,8 +1,9 @@
 """GPU parity of snap_prefill (causal prefill attention with the SnapKV window
 statistics taken from the attention pass, then the compression) against the
-fp64 oracle: the attention output of every position, and the compression
-result (selection, pooled scores, cache bytes, metadata) for the observation
-window formed by the last w prompt queries.
+fp64 oracle: the attention output of every position, within the error bf16
+arithmetic allows (attention_bound), and the compression result (selection,
+pooled scores, cache bytes, metadata) for the observation window formed by
+the last w prompt queries.
 
 Every case prints what names it before touching the GPU.
 """
@@ -13,7 +14,7 @@ import torch
 import oracle
 import paper_2511_03092_amd as snap
 import synth
-from snaphelp import (ALL_RTOL, DECISION_RTOL, NEAR_RTOL, TOL, GpuCache, check_compress, check_selection,
+from snaphelp import (ALL_RTOL, DECISION_RTOL, NEAR_RTOL, GpuCache, check_compress, check_selection,
                       oracle_params, params_of, score_errors)
 
 pytestmark = pytest.mark.gpu
@@ -45,27 +46,50 @@ def _gpu_prefill(p, wl, lengths, slots, n_slots, max_len=None, salt=0):
     return q, k, v, cache, out, sel.cpu().numpy(), pooled.cpu().numpy()
 
 
+# bf16's unit roundoff (8-bit significand, rounding to nearest)
+U_BF16 = 2.0 ** -8
+
+
+def attention_bound(exp, exp_absv):
+    """The largest error a bf16 attention output may carry, element by element:
+    the probabilities enter the P V product rounded to bf16 (each within u,
+    relative) and the output is stored in bf16 (within u, relative), so
+    |got - exp| <= u (|exp| + sum_j p_j |v_j|) (1 + 2u), where sum_j p_j |v_j| is
+    the oracle's attention over |v|; 1e-5 covers the fp32 logits and sums."""
+    return U_BF16 * (np.abs(exp) + exp_absv) * (1 + 2 * U_BF16) + 1e-5
+
+
 def _check_attention(p, lengths, q, k, v, out):
+    """Every output position against the oracle within attention_bound (the
+    attention over |v| is formed for the sequences whose error the |exp| term
+    alone does not cover).  Returns the largest absolute error and the largest
+    ratio of error to bound."""
     op = oracle_params(p)
     exp = oracle.prefill_attn(op, lengths, q, k, v)
-    worst = 0.0
+    worst, worst_ratio = 0.0, 0.0
     for b, L in enumerate(lengths):
-        got = out[b, :, :L].double().cpu().numpy()
-        err = float(np.max(np.abs(got - exp[b]))) if L else 0.0
-        worst = max(worst, err)
-        assert err <= TOL["bf16"], (b, L, err)
         assert torch.all(torch.isnan(out[b, :, L:].float())), f"rows past L={L} written"
-    return worst
+        if not L:
+            continue
+        got = out[b, :, :L].double().cpu().numpy()
+        err = np.abs(got - exp[b])
+        absv = 0.0
+        if not np.all(err <= attention_bound(exp[b], 0.0)):
+            absv = oracle.prefill_attn(op, [L], q[b:b + 1], k[b:b + 1], np.abs(oracle.f64(v[b:b + 1])))[0]
+        ratio = float(np.max(err / attention_bound(exp[b], absv)))
+        assert ratio <= 1.0, (b, L, float(np.max(err)), ratio)
+        worst, worst_ratio = max(worst, float(np.max(err))), max(worst_ratio, ratio)
+    return worst, worst_ratio
 
 
 def _run(wl, p, lengths, slots=None, n_slots=None, near_rtol=NEAR_RTOL, max_len=None):
     slots = list(range(len(lengths))) if slots is None else slots
     n_slots = len(lengths) if n_slots is None else n_slots
     q, k, v, cache, out, sel, pooled = _gpu_prefill(p, wl, lengths, slots, n_slots, max_len=max_len)
-    err = _check_attention(p, lengths, q, k, v, out)
+    err, ratio = _check_attention(p, lengths, q, k, v, out)
     qobs = oracle.window_queries(oracle_params(p), lengths, q)
     st = check_compress(p, cache, qobs, k, v, lengths, slots, sel, pooled)
-    print(f"  attention max abs err {err:.3e}; swaps {st['swaps']}, pooled max rel err "
+    print(f"  attention max abs err {err:.3e} ({ratio:.2f} of the bf16 bound); swaps {st['swaps']}, pooled max rel err "
           f"{st['pooled_rel_err']:.3e}, decision band {st['decision_rel_err']:.3e}, near band "
           f"{st['near_rel_err']:.3e}", flush=True)
     assert st["decision_rel_err"] <= DECISION_RTOL and st["near_rel_err"] <= near_rtol
@@ -143,10 +167,12 @@ def _sampled_rows(p, qc, kc, vc, out, L, rows, heads):
             qq = np.zeros((1, i + 1, p.d_qk))
             qq[0, i] = qc[h, i]
             exp = oracle.prefill_attn_group(op, i + 1, qq, kc[g, :i + 1], vc[g, :i + 1], rows=(i, i + 1))
+            expa = oracle.prefill_attn_group(op, i + 1, qq, kc[g, :i + 1], np.abs(vc[g, :i + 1]), rows=(i, i + 1))
             got = out[h, i].double().cpu().numpy()
-            err = float(np.max(np.abs(got - exp[0, 0])))
+            e = np.abs(got - exp[0, 0])
+            err = float(np.max(e))
             worst = max(worst, err)
-            assert err <= TOL["bf16"], (h, i, err)
+            assert np.all(e <= attention_bound(exp[0, 0], expa[0, 0])), (h, i, err)
     return worst
 
 
