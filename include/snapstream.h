@@ -117,7 +117,8 @@ typedef struct {
   int32_t in_dtype;    /* q / k / v inputs: SNAP_F32 or SNAP_BF16                */
   int32_t kv_dtype;    /* cache storage: SNAP_F32, SNAP_BF16 (in_dtype == the
                           same) or SNAP_FP8_E4M3 (with SNAP_BF16 inputs)          */
-  float sm_scale;      /* softmax scale; <= 0 means 1/sqrt(d_qk)                 */
+  float sm_scale;      /* softmax scale; <= 0 means 1/sqrt(d_qk); a positive
+                          value must be finite and at least 1e-30                */
   int32_t fp8_scales;  /* snap_fp8_scales (fp8 caches; ignored otherwise)        */
   int32_t fp8_qk;      /* decode attention over an fp8 cache: 0 = Q K^T in bf16
                           (the codes converted exactly); 1 = the query of each

@@ -54,6 +54,10 @@ static snap_status check_params(const snap_params* p) {
   if (p->pool != SNAP_POOL_MAX && p->pool != SNAP_POOL_AVG) return fail(SNAP_ERR_INVALID_ARG, "unknown pool type");
   if (p->norm != SNAP_NORM_CAND && p->norm != SNAP_NORM_ROW) return fail(SNAP_ERR_INVALID_ARG, "unknown norm");
   if (!isfinite(p->sm_scale)) return fail(SNAP_ERR_INVALID_ARG, "sm_scale must be finite");
+  // a positive scale must keep scale * log2(e) a normal fp32 value: the score
+  // kernels form every logit from it and its remainder
+  if (p->sm_scale > 0.f && p->sm_scale < 1e-30f)
+    return fail(SNAP_ERR_INVALID_ARG, "sm_scale must be <= 0 (the default) or at least 1e-30");
   if (p->fp8_scales != SNAP_FP8_SCALES_GIVEN && p->fp8_scales != SNAP_FP8_SCALES_AMAX)
     return fail(SNAP_ERR_INVALID_ARG, "unknown fp8_scales mode");
   if (p->fp8_qk != 0 && p->fp8_qk != 1) return fail(SNAP_ERR_INVALID_ARG, "fp8_qk must be 0 or 1");

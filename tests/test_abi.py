@@ -89,6 +89,8 @@ def _compress_status(p, ws_bytes=1 << 30, **kw):
     (dict(in_dtype=snap.SNAP_F32, kv_dtype=snap.SNAP_BF16), snap.SNAP_ERR_UNSUPPORTED),
     (dict(obs_window=128), snap.SNAP_ERR_UNSUPPORTED),
     (dict(norm=5), snap.SNAP_ERR_INVALID_ARG),
+    (dict(sm_scale=1e-31), snap.SNAP_ERR_INVALID_ARG),
+    (dict(sm_scale=float("inf")), snap.SNAP_ERR_INVALID_ARG),
 ])
 def test_invalid_params_rejected(bad, code):
     st, msg = _compress_status(_params(**bad))
