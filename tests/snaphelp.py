@@ -396,7 +396,8 @@ def decode_steps(p: snap.Params, wl: synth.Workload, cache: GpuCache, slots, ste
 
 
 def run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=float("nan"), layer=0, salt=0,
-             check_every=1, fp8_scales=False, near_rtol=NEAR_RTOL, all_rtol=ALL_RTOL, fused=False, poison=True):
+             check_every=1, fp8_scales=False, near_rtol=NEAR_RTOL, all_rtol=ALL_RTOL, fused=False, poison=True,
+             score_rtol_factor=1.0):
     """Compress a padded batch into `slots` of an n_slots cache, check it
     against the oracle (selection, pooled scores, cache bytes, untouched
     slots), refill the rows decode must not read with the canary, then run
@@ -426,9 +427,11 @@ def run_case(wl, p, lengths, slots, n_slots, steps, out_dtype, tol, pad_value=fl
     print(f"  swaps within tolerance: {stats['swaps']}; pooled-score rel err: decision band "
           f"{stats['decision_rel_err']:.3e}, near band {stats['near_rel_err']:.3e}, anywhere "
           f"{stats['pooled_rel_err']:.3e}", flush=True)
-    assert stats["decision_rel_err"] <= DECISION_RTOL
-    assert stats["near_rel_err"] <= near_rtol
-    assert stats["pooled_rel_err"] <= all_rtol
+    # score_rtol_factor: logits larger than the default scale's by this
+    # factor (a caller's sm_scale), whose fp32 rounding grows with them
+    assert stats["decision_rel_err"] <= DECISION_RTOL * score_rtol_factor
+    assert stats["near_rel_err"] <= near_rtol * score_rtol_factor
+    assert stats["pooled_rel_err"] <= all_rtol * score_rtol_factor
     err = 0.0
     if steps:
         if poison:

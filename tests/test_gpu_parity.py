@@ -94,6 +94,23 @@ POLICIES = {
 }
 
 
+@pytest.mark.parametrize("scale", [0.3, 0.02])
+def test_caller_softmax_scale(scale):
+    """A softmax scale the caller sets (sm_scale > 0) in place of 1/sqrt(d):
+    0.3 gives logits 3.4 times the default's, 0.02 flattens the softmax.
+    Compression and decode against the oracle with the same scale (Eq. 3,
+    Sec. III-C).  The pooled scores' fp32 error comes from the rounding of
+    the logits (it is proportional to their magnitude), so the score bounds,
+    set for the default scale, grow by sm_scale * sqrt(d) when that exceeds
+    1; the selection rule and the decode bound do not change."""
+    wl = synth.small(MED, topk=200)
+    p = params_of(wl, sm_scale=scale)
+    lengths = [4000, 1500]
+    factor = max(1.0, scale * wl.d_qk ** 0.5)
+    _announce(f"sm_scale {scale}: G=4 D=128, lengths {lengths}, 16 decode steps, score bounds x{factor:.2f}")
+    _run_case(wl, p, lengths, [1, 0], 2, 16, torch.bfloat16, TOL["bf16"], score_rtol_factor=factor)
+
+
 @pytest.mark.parametrize("name", list(POLICIES))
 def test_selection_policies(name):
     make, lengths, steps, every, band = POLICIES[name]
