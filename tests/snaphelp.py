@@ -35,9 +35,9 @@ TOL = {"f32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
 #    fp32 logits from the MFMA accumulation, the column-sum and pooling trees);
 #    the looser bound applies when a key's score sums fewer than 8 weights
 #    (G * w < 8), where one logit's rounding is not averaged down;
-# These two bounds are the measured size of those errors (random
-# configurations beside this suite have exceeded them rarely, always with the
-# selection exact), not worst cases: the anywhere bound covers those.
+# These two bounds are the measured size of those errors, not worst cases:
+# random configurations beside this suite have exceeded them rarely, always
+# with the selection exact.
 #  * anywhere -- large planted logits carry the most fp32 rounding.
 DECISION_RTOL = 5e-7
 DECISION_RTOL_BAND = 2.0 ** -19
