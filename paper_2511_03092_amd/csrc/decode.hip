@@ -1084,6 +1084,86 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
     ((float*)a.out)[oi] = o;
 }
 
+// ---------------------------------------------------------------- merge of many chunks
+// The same merge as combine for calls split into more chunks than combine
+// keeps in registers (a small batch spread over every CU in short chunks):
+// one 256-thread workgroup per (sequence, query head).  Thread t takes the
+// value dims 4*(t % DG) .. 4*(t % DG) + 3 of chunks t / DG, t / DG + CL, ...;
+// every partial and (m, l) load it needs is issued before the first is used,
+// it merges its chunks against their largest reference, and the CL merges of
+// each dim group are merged once more through LDS.  The slot id is tested
+// after the barrier, so its load and the partial loads are in flight together
+// (a skipped slot's workgroup merges what its workspace rows hold and stores
+// nothing).
+constexpr int kMergeThreads = 256;
+constexpr int kMergeMaxChunks = 128;
+
+template <int DV>
+__global__ __launch_bounds__(kMergeThreads) void merge_chunks(CombineArgs a) {
+  constexpr int DG = DV / 4;                 // float4 groups of a partial row
+  constexpr int CL = kMergeThreads / DG;     // chunk lanes
+  constexpr int PER = kMergeMaxChunks / CL;  // chunks per thread, at most
+  __shared__ float4 sacc[kMergeThreads];
+  __shared__ float2 sml[kMergeThreads];
+  const int bh = bid_x(), b = bh / a.Hq;
+  const int slot = a.slot_ids[b];
+  if (!debug_check(a.n_chunks <= kMergeMaxChunks && a.dv == DV, kDbgCombine)) return;
+  const int t = tid(), dg = t % DG, cl = t / DG;
+  const float4* part = (const float4*)(a.part + (size_t)bh * a.n_chunks * DV) + dg;
+  const float2* ml = a.ml + (size_t)bh * a.n_chunks;
+  float4 pv[PER];
+  float2 mv[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int c = cl + CL * i;
+    pv[i] = c < a.n_chunks ? part[(size_t)c * DG] : make_float4(0.f, 0.f, 0.f, 0.f);
+    mv[i] = c < a.n_chunks ? ml[c] : make_float2(-INFINITY, 0.f);
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) m = fmaxf(m, mv[i].x);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float l = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const float w = mv[i].x == -INFINITY ? 0.f : fast_exp2(mv[i].x - m);
+    acc.x = fmaf(w, pv[i].x, acc.x);
+    acc.y = fmaf(w, pv[i].y, acc.y);
+    acc.z = fmaf(w, pv[i].z, acc.z);
+    acc.w = fmaf(w, pv[i].w, acc.w);
+    l = fmaf(w, mv[i].y, l);
+  }
+  sacc[t] = acc;
+  sml[t] = make_float2(m, l);
+  __syncthreads();
+  if (cl != 0 || slot < 0 || slot >= a.n_slots) return;
+  float M = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < CL; ++j) M = fmaxf(M, sml[dg + DG * j].x);
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  float L = 0.f;
+#pragma unroll
+  for (int j = 0; j < CL; ++j) {
+    const float2 mj = sml[dg + DG * j];
+    const float w = mj.x == -INFINITY ? 0.f : fast_exp2(mj.x - M);
+    const float4 aj = sacc[dg + DG * j];
+    o.x = fmaf(w, aj.x, o.x);
+    o.y = fmaf(w, aj.y, o.y);
+    o.z = fmaf(w, aj.z, o.z);
+    o.w = fmaf(w, aj.w, o.w);
+    L = fmaf(w, mj.y, L);
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const size_t oi = (size_t)bh * DV + 4 * dg;
+  if (a.out_bf16) {
+    const u32x2 w2 = {f32_to_bf16_bits(o.x * inv) | (f32_to_bf16_bits(o.y * inv) << 16),
+                      f32_to_bf16_bits(o.z * inv) | (f32_to_bf16_bits(o.w * inv) << 16)};
+    *(u32x2*)((uint16_t*)a.out + oi) = w2;
+  } else {
+    *(float4*)((float*)a.out + oi) = make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
+  }
+}
+
 // ---------------------------------------------------------------- append / advance
 struct AppendArgs {
   const void* k_new;  // [n][Hkv][dk]
@@ -1178,15 +1258,20 @@ Geometry decode_geometry(const snap_params& p, int n) {
   const bool latent = p.v_in_k && p.d_qk == 576;
   const bool latent_lds = latent && p.kv_dtype == SNAP_BF16;  // one 4-wave workgroup per CU (LDS-bound)
   const int target = latent_lds ? kLatentLdsWGs : (latent ? 512 : 2048);
-  const int min_rows = latent ? 256 : 128;
   // rounded down: a grid just above the resident capacity would leave a
   // partial second round of workgroups (measured 25% slower on the fp8 GQA
   // kernel at 248 units: 9 chunks against 8)
-  int want = target / units;
+  const int want = target / units;
+  // a small GQA batch (more chunks wanted than combine keeps in registers)
+  // splits into chunks as short as one 32-row block, up to what merge_chunks
+  // holds, so that a launch-bound call spreads over more waves
+  const bool many = !latent && want > kCombineRegChunks;
+  const int min_rows = latent ? 256 : (many ? 32 : 128);
   int maxc = (B + min_rows - 1) / min_rows;
   if (maxc < 1) maxc = 1;
-  if (maxc > kMaxChunks) maxc = kMaxChunks;
+  if (maxc > (many ? kMergeMaxChunks : kMaxChunks)) maxc = many ? kMergeMaxChunks : kMaxChunks;
   g.n_chunks = want < 1 ? 1 : (want > maxc ? maxc : want);
+  g.merge_many = many && g.n_chunks > kCombineRegChunks;
   size_t off = 0;
   g.off_part = off;
   off = align256(off + (size_t)(n > 0 ? n : 1) * p.n_q_heads * g.n_chunks * p.d_v * sizeof(float));
@@ -1287,8 +1372,13 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
   ca.n_chunks = geo.n_chunks;
   ca.n_slots = c.n_slots;
   ca.out_bf16 = out_dtype == SNAP_BF16;
-  hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads, (p.d_v + kCombineThreads - 1) / kCombineThreads),
-                     dim3(kCombineThreads), 0, stream, ca);
+  if (geo.merge_many && p.d_v == 128)
+    hipLaunchKernelGGL(merge_chunks<128>, dim3(n * p.n_q_heads), dim3(kMergeThreads), 0, stream, ca);
+  else if (geo.merge_many)
+    hipLaunchKernelGGL(merge_chunks<64>, dim3(n * p.n_q_heads), dim3(kMergeThreads), 0, stream, ca);
+  else
+    hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads, (p.d_v + kCombineThreads - 1) / kCombineThreads),
+                       dim3(kCombineThreads), 0, stream, ca);
   if (hipGetLastError() != hipSuccess) return SNAP_ERR_HIP;
   return SNAP_OK;
 }

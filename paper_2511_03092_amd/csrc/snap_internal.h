@@ -160,6 +160,7 @@ struct Geometry {
   size_t prefill_bytes;
   // decode
   int n_chunks;     // split-K chunks per (sequence, KV head)
+  bool merge_many;  // the chunks are merged by merge_chunks (more than the combine keeps in registers)
   size_t off_part, off_ml;
   size_t decode_bytes;
 };
