@@ -1087,8 +1087,10 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
 // ---------------------------------------------------------------- merge of many chunks
 // The same merge as combine for calls split into more chunks than combine
 // keeps in registers (a small batch spread over every CU in short chunks):
-// one 256-thread workgroup per (sequence, query head).  Thread t takes the
-// value dims 4*(t % DG) .. 4*(t % DG) + 3 of chunks t / DG, t / DG + CL, ...;
+// one 256-thread workgroup per (sequence, query head) and slice of DV value
+// dims (d_v / DV slices: one, or four for 512-wide latent rows).  Thread t
+// takes the slice's dims 4*(t % DG) .. 4*(t % DG) + 3 of chunks t / DG,
+// t / DG + CL, ...;
 // every partial and (m, l) load it needs is issued before the first is used,
 // it merges its chunks against their largest reference, and the CL merges of
 // each dim group are merged once more through LDS.  The slot id is tested
@@ -1107,16 +1109,18 @@ __global__ __launch_bounds__(kMergeThreads) void merge_chunks(CombineArgs a) {
   __shared__ float2 sml[kMergeThreads];
   const int bh = bid_x(), b = bh / a.Hq;
   const int slot = a.slot_ids[b];
-  if (!debug_check(a.n_chunks <= kMergeMaxChunks && a.dv == DV, kDbgCombine)) return;
+  if (!debug_check(a.n_chunks <= kMergeMaxChunks && a.dv % DV == 0, kDbgCombine)) return;
   const int t = tid(), dg = t % DG, cl = t / DG;
-  const float4* part = (const float4*)(a.part + (size_t)bh * a.n_chunks * DV) + dg;
+  const int d0 = bid_y() * DV;  // first value dim of the slice
+  const int RG = a.dv / 4;      // float4 groups of a whole partial row
+  const float4* part = (const float4*)(a.part + (size_t)bh * a.n_chunks * a.dv + d0) + dg;
   const float2* ml = a.ml + (size_t)bh * a.n_chunks;
   float4 pv[PER];
   float2 mv[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int c = cl + CL * i;
-    pv[i] = c < a.n_chunks ? part[(size_t)c * DG] : make_float4(0.f, 0.f, 0.f, 0.f);
+    pv[i] = c < a.n_chunks ? part[(size_t)c * RG] : make_float4(0.f, 0.f, 0.f, 0.f);
     mv[i] = c < a.n_chunks ? ml[c] : make_float2(-INFINITY, 0.f);
   }
   float m = -INFINITY;
@@ -1154,7 +1158,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_chunks(CombineArgs a) {
     L = fmaf(w, mj.y, L);
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  const size_t oi = (size_t)bh * DV + 4 * dg;
+  const size_t oi = (size_t)bh * a.dv + d0 + 4 * dg;
   if (a.out_bf16) {
     const u32x2 w2 = {f32_to_bf16_bits(o.x * inv) | (f32_to_bf16_bits(o.y * inv) << 16),
                       f32_to_bf16_bits(o.z * inv) | (f32_to_bf16_bits(o.w * inv) << 16)};
@@ -1271,7 +1275,10 @@ Geometry decode_geometry(const snap_params& p, int n) {
   if (maxc < 1) maxc = 1;
   if (maxc > (many ? kMergeMaxChunks : kMaxChunks)) maxc = many ? kMergeMaxChunks : kMaxChunks;
   g.n_chunks = want < 1 ? 1 : (want > maxc ? maxc : want);
-  g.merge_many = many && g.n_chunks > kCombineRegChunks;
+  // more chunks than combine keeps in registers (small batches; also a few
+  // latent sequences, whose chunks are never shorter than 256 rows) go to
+  // merge_chunks
+  g.merge_many = g.n_chunks > kCombineRegChunks && g.n_chunks <= kMergeMaxChunks;
   size_t off = 0;
   g.off_part = off;
   off = align256(off + (size_t)(n > 0 ? n : 1) * p.n_q_heads * g.n_chunks * p.d_v * sizeof(float));
@@ -1372,10 +1379,10 @@ snap_status launch_decode(const snap_params& p, const snap_cache& c, const int32
   ca.n_chunks = geo.n_chunks;
   ca.n_slots = c.n_slots;
   ca.out_bf16 = out_dtype == SNAP_BF16;
-  if (geo.merge_many && p.d_v == 128)
-    hipLaunchKernelGGL(merge_chunks<128>, dim3(n * p.n_q_heads), dim3(kMergeThreads), 0, stream, ca);
-  else if (geo.merge_many)
+  if (geo.merge_many && p.d_v == 64)
     hipLaunchKernelGGL(merge_chunks<64>, dim3(n * p.n_q_heads), dim3(kMergeThreads), 0, stream, ca);
+  else if (geo.merge_many)  // d_v = 128 or 512: 128-dim slices
+    hipLaunchKernelGGL(merge_chunks<128>, dim3(n * p.n_q_heads, p.d_v / 128), dim3(kMergeThreads), 0, stream, ca);
   else
     hipLaunchKernelGGL(combine, dim3(n * p.n_q_heads, (p.d_v + kCombineThreads - 1) / kCombineThreads),
                        dim3(kCombineThreads), 0, stream, ca);

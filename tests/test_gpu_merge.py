@@ -59,6 +59,28 @@ CASES = [
 ]
 
 
+# Latent caches (576-wide rows, values = the first 512 dims) keep chunks of at
+# least 256 rows; one or two sequences with a budget above 32 such chunks are
+# merged by merge_chunks in four 128-dim slices.
+LATENT_CASES = [
+    ("latent-bf16-36", "bf16", [9500], [0], 1, torch.bfloat16, 36),
+    ("latent-fp8-36", "fp8", [9400, 3000], [1, 0], 2, torch.float32, 36),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", LATENT_CASES, ids=[c[0] for c in LATENT_CASES])
+def test_many_chunk_latent_decode(case):
+    name, kv, lengths, slots, n_slots, out_dtype, want = case
+    wl = synth.small(synth.WORKLOADS["mla-8head-61layer-b16-128k"], sink=4, recent=60, topk=9000, kv_dtype=kv,
+                     batch=len(lengths))
+    p = params_of(wl, fp8_scales=snap.SNAP_FP8_SCALES_AMAX) if kv == "fp8" else params_of(wl)
+    assert n_chunks_of(p, len(lengths)) == want
+    print(f"\n[case] merge {name}: latent, cache {kv}, budget 4+60+9000, lengths {lengths} -> slots {slots} "
+          f"of {n_slots}, {want} chunks", flush=True)
+    run_case(wl, p, lengths, slots, n_slots, 6, out_dtype, TOL[kv], near_rtol=NEAR_RTOL, fused="alt")
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_many_chunk_decode(case):
