@@ -1210,7 +1210,8 @@ __device__ __forceinline__ Raw8In<In> load8(const In* src) {
   return x;
 }
 // ... stored into the cache, quantised to E4M3 codes of x / scale when the
-// cache is fp8.
+// cache is fp8 (the correctly rounded quotient, then the conversion
+// instruction: e4m3x4_hw).
 template <typename In, typename Out>
 __device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scale, float inv) {
   if constexpr (sizeof(Out) == 1) {
@@ -1225,14 +1226,12 @@ __device__ __forceinline__ void store8(const Raw8In<In>& x, Out* dst, float scal
 #pragma unroll
       for (int i = 0; i < 8; ++i) f[i] = __uint_as_float(x.w[i >> 2][i & 3]);
     }
+    float qv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qv[i] = div_by_scale(f[i], scale, inv);
     u32x2 o;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint32_t w = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) w |= f32_to_e4m3(div_by_scale(f[h * 4 + i], scale, inv)) << (8 * i);
-      o[h] = w;
-    }
+    o[0] = e4m3x4_hw(qv[0], qv[1], qv[2], qv[3]);
+    o[1] = e4m3x4_hw(qv[4], qv[5], qv[6], qv[7]);
     __builtin_nontemporal_store(o, (u32x2*)dst);
   } else {
 #pragma unroll
