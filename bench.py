@@ -396,7 +396,7 @@ def main(args):
                        "counters": measured_mfma(wl.name)},
         "roofline": {"bound": "hbm",
                      "kernel": ("snap_cache_append + snap_decode_attn" if args.two_calls else
-                                "snap_decode_step (append + split-K attention, one launch) + combine"),
+                                "snap_decode_step (append + split-K attention, one launch) + chunk merge"),
                      "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(wl.name),
                      "algorithmic_bytes_per_launch": dec_bytes},
@@ -616,7 +616,7 @@ def run_cb(args, wl):
                        "mfma_util_lower_bound": round(score_tflops / PEAK_BF16_TFLOPS, 4),
                        "counters": measured_mfma(wl.name)},
         "roofline": {"bound": "hbm",
-                     "kernel": "snap_decode_step (fp8 cache: append + split-K attention, one launch) + combine"
+                     "kernel": "snap_decode_step (fp8 cache: append + split-K attention, one launch) + chunk merge"
                                + (", fp8 Q K^T" if args.fp8_qk else ""),
                      "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),

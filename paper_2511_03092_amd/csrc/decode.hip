@@ -1084,9 +1084,11 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
     ((float*)a.out)[oi] = o;
 }
 
-// ---------------------------------------------------------------- merge of many chunks
-// The same merge as combine for calls split into more chunks than combine
-// keeps in registers (a small batch spread over every CU in short chunks):
+// ---------------------------------------------------------------- merge of the chunks
+// The same merge as combine, with every load in flight at once: for calls of
+// up to 16 chunks (the 128k batches' 8 and 16) and for calls split into more
+// chunks than combine keeps in registers (a small batch spread over every CU
+// in short chunks):
 // one 256-thread workgroup per (sequence, query head) and slice of DV value
 // dims (d_v / DV slices: one, or four for 512-wide latent rows).  Thread t
 // takes the slice's dims 4*(t % DG) .. 4*(t % DG) + 3 of chunks t / DG,
@@ -1275,10 +1277,11 @@ Geometry decode_geometry(const snap_params& p, int n) {
   if (maxc < 1) maxc = 1;
   if (maxc > (many ? kMergeMaxChunks : kMaxChunks)) maxc = many ? kMergeMaxChunks : kMaxChunks;
   g.n_chunks = want < 1 ? 1 : (want > maxc ? maxc : want);
-  // more chunks than combine keeps in registers (small batches; also a few
-  // latent sequences, whose chunks are never shorter than 256 rows) go to
-  // merge_chunks
-  g.merge_many = g.n_chunks > kCombineRegChunks && g.n_chunks <= kMergeMaxChunks;
+  // merge_chunks takes every call of at most 16 chunks and of 33 to 128
+  // (small batches; also a few latent sequences, whose chunks are never
+  // shorter than 256 rows); combine takes 17 to 32 chunks, where it measured
+  // faster (the 8-sequence GQA batch's 32 chunks: 3%), and more than 128
+  g.merge_many = (g.n_chunks <= 16 || g.n_chunks > kCombineRegChunks) && g.n_chunks <= kMergeMaxChunks;
   size_t off = 0;
   g.off_part = off;
   off = align256(off + (size_t)(n > 0 ? n : 1) * p.n_q_heads * g.n_chunks * p.d_v * sizeof(float));
