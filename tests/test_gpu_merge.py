@@ -1,13 +1,15 @@
 """Split-K decode of small batches (Sec. III-C: attention over the compressed
 cache, split into chunks merged by log-sum-exp).  A call with few (sequence,
 KV head) units is split into chunks as short as one 32-row block, up to 128
-per unit, and when that is more chunks than the combine kernel keeps in
-registers (32) they are merged by merge_chunks.  The host test pins which
-calls take which path, from the workspace size (which holds the partials of
-every chunk); the GPU tests run compress and decode steps of such calls
-against the oracle, for both value widths (64, 128), both output dtypes,
-bf16, fp32 and fp8 caches, chunks left empty by short prompts and a slot id
-the call must skip.
+per unit; merge_chunks merges calls of 33 to 128 chunks per unit (more than
+the combine kernel keeps in registers) as well as those of at most 16, and
+the combine those of 17 to 32.  The host test pins the chunk counts of the
+benchmark shapes, from the workspace size (which holds the partials of every
+chunk); the GPU tests run compress and decode steps of calls with 33 to 128
+chunks against the oracle, for both value widths (64, 128) and the latent
+512, both output dtypes, bf16, fp32 and fp8 caches, chunks left empty by
+short prompts and a slot id the call must skip.  (Calls of at most 16 chunks
+run through merge_chunks in the rest of the GPU suite.)
 """
 import pytest
 import torch
