@@ -1085,20 +1085,18 @@ __global__ __launch_bounds__(kCombineThreads) void combine(CombineArgs a) {
 }
 
 // ---------------------------------------------------------------- merge of the chunks
-// The same merge as combine, with every load in flight at once: for calls of
+// The same merge as combine, with every load in flight at once, for calls of
 // up to 16 chunks (the 128k batches' 8 and 16) and for calls split into more
 // chunks than combine keeps in registers (a small batch spread over every CU
-// in short chunks):
-// one 256-thread workgroup per (sequence, query head) and slice of DV value
-// dims (d_v / DV slices: one, or four for 512-wide latent rows).  Thread t
-// takes the slice's dims 4*(t % DG) .. 4*(t % DG) + 3 of chunks t / DG,
-// t / DG + CL, ...;
-// every partial and (m, l) load it needs is issued before the first is used,
-// it merges its chunks against their largest reference, and the CL merges of
-// each dim group are merged once more through LDS.  The slot id is tested
-// after the barrier, so its load and the partial loads are in flight together
-// (a skipped slot's workgroup merges what its workspace rows hold and stores
-// nothing).
+// in short chunks).  One 256-thread workgroup per (sequence, query head) and
+// slice of DV value dims (d_v / DV slices: one, or four for 512-wide latent
+// rows).  Thread t takes the slice's dims 4*(t % DG) .. 4*(t % DG) + 3 of
+// chunks t / DG, t / DG + CL, ...: every partial and (m, l) load it needs is
+// issued before the first is used, it merges its chunks against their
+// largest reference, and the CL merges of each dim group are merged once
+// more through LDS.  The slot id is tested after the barrier, so its load and
+// the partial loads are in flight together (a skipped slot's workgroup merges
+// what its workspace rows hold and stores nothing).
 constexpr int kMergeThreads = 256;
 constexpr int kMergeMaxChunks = 128;
 
